@@ -1,0 +1,77 @@
+"""Per-head dynamic absmax quantization to e4m3fn (test oracle).
+
+Eq. (2) of the paper (Sec. 3): for each head h of a tensor X,
+    s_X^(h) = max_{i,j} |X^(h)_ij| / 448,
+    X_8     = rn_fp8( clamp(X / s_X, -448, 448) ),
+with an FP32 dequantization scale, so that X ~= s_X * X_8.  The scale is
+computed from the tensor itself (no calibration).  In the ICL layer keys and
+values come from the train rows only, and the test queries are quantized
+with the scale of the *train* queries, which makes test predictions
+independent of the test batch (Sec. 3, paragraph after Eq. (2); Table 1,
+last row).
+
+Readings where the paper is silent (each also listed in the design notes):
+* granularity: one scale per (table b, head h), over all rows and channels;
+* ``s = fl32(amax / 448)`` and ``y = fl32(x / s)`` are IEEE fp32 divisions
+  (round to nearest even) -- the formula read literally;
+* the clamp is applied before rounding, so values beyond the train amax
+  (possible only for test queries) saturate to +-448;
+* ``amax == 0`` (or an amax whose quotient underflows to 0) uses s = 1, which
+  maps the whole head to zero codes;
+* negative values that round to zero keep their sign (code 0x80).
+
+Layouts: inputs are (B, S, H, D) row-major (rows, heads, head_dim per table,
+as the paper writes activations X in R^{S x H x d}); codes are returned as
+(B, H, S, D) uint8 and scales as (B, H) float32.
+"""
+import numpy as np
+
+from .e4m3 import encode_rne, MAX_FINITE
+
+F32_448 = np.float32(448.0)
+
+
+def absmax_per_head(x):
+    """max |x| over rows and channels, per (b, h): (B,S,H,D) -> (B,H) float32."""
+    x = np.asarray(x, dtype=np.float32)
+    if x.shape[1] == 0:
+        return np.zeros((x.shape[0], x.shape[2]), dtype=np.float32)
+    return np.abs(x).max(axis=(1, 3)).astype(np.float32)
+
+
+def scale_from_amax(amax):
+    """Dequantization scale s = fl32(amax / 448); s = 1 where that is 0."""
+    s = np.divide(np.asarray(amax, dtype=np.float32), F32_448, dtype=np.float32)
+    return np.where(s == 0, np.float32(1.0), s).astype(np.float32)
+
+
+def quantize_with_scale(x, s):
+    """Codes rn_fp8(clamp(fl32(x / s), -448, 448)): (B,S,H,D), (B,H) -> (B,H,S,D) uint8."""
+    x = np.asarray(x, dtype=np.float32)
+    s = np.asarray(s, dtype=np.float32)
+    y = np.divide(x, s[:, None, :, None], dtype=np.float32)
+    y = np.clip(y, -MAX_FINITE, MAX_FINITE)
+    codes = encode_rne(y)
+    return np.ascontiguousarray(codes.transpose(0, 2, 1, 3))
+
+
+def quantize_qkv_per_head(q_train, k, v, q_test=None):
+    """Eq. (2) applied to the ICL layer's tensors.
+
+    Q_train, K and V get their own per-head scales; Q_test (optional) is
+    quantized with the scale of Q_train.  Returns a dict with the codes
+    ``q8_train, k8, v8, q8_test`` ((B,H,S,D) uint8) and the scales
+    ``s_q, s_k, s_v`` ((B,H) float32).
+    """
+    s_q = scale_from_amax(absmax_per_head(q_train))
+    s_k = scale_from_amax(absmax_per_head(k))
+    s_v = scale_from_amax(absmax_per_head(v))
+    out = {
+        "q8_train": quantize_with_scale(q_train, s_q),
+        "k8": quantize_with_scale(k, s_k),
+        "v8": quantize_with_scale(v, s_v),
+        "s_q": s_q, "s_k": s_k, "s_v": s_v,
+    }
+    if q_test is not None:
+        out["q8_test"] = quantize_with_scale(q_test, s_q)
+    return out

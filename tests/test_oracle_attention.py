@@ -1,0 +1,164 @@
+"""Pins of the oracle's attention references: brute force, a library SDPA,
+closed forms, and the exact-arithmetic limit of the one-pass kernel model."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as A
+from oracle import quantize as Q
+from oracle.e4m3 import decode, encode_rne
+
+
+def brute_force_attention(q, k, v, alpha):
+    out = []
+    for qi in q:
+        logits = [alpha * sum(a * b for a, b in zip(qi, kj)) for kj in k]
+        mx = max(logits)
+        w = [math.exp(t - mx) for t in logits]
+        z = sum(w)
+        out.append([sum(wj * vj[c] for wj, vj in zip(w, v)) / z for c in range(len(v[0]))])
+    return np.array(out)
+
+
+@pytest.mark.parametrize("R,N,D", [(1, 1, 1), (3, 5, 2), (8, 8, 4), (2, 7, 3)])
+def test_softmax_attention_matches_brute_force(R, N, D):
+    rng = np.random.default_rng(R * 100 + N * 10 + D)
+    q, k, v = rng.standard_normal((R, D)), rng.standard_normal((N, D)), rng.standard_normal((N, D))
+    ours = A.softmax_attention(q, k, v, 0.7)
+    ref = brute_force_attention(q.tolist(), k.tolist(), v.tolist(), 0.7)
+    assert np.allclose(ours, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_softmax_attention_matches_torch_sdpa_fp64():
+    rng = np.random.default_rng(11)
+    q, k, v = rng.standard_normal((70, 64)) * 3, rng.standard_normal((300, 64)) * 3, rng.standard_normal((300, 64))
+    ref = torch.nn.functional.scaled_dot_product_attention(
+        torch.from_numpy(q)[None], torch.from_numpy(k)[None], torch.from_numpy(v)[None], scale=0.125)[0].numpy()
+    ours = A.softmax_attention(q, k, v, 0.125, chunk_rows=16)
+    assert np.allclose(ours, ref, rtol=1e-11, atol=1e-12)
+
+
+def test_rows_sum_to_one_constant_v_and_identical_keys():
+    rng = np.random.default_rng(12)
+    q, k = rng.standard_normal((20, 16)) * 5, rng.standard_normal((40, 16)) * 5
+    ones = np.ones((40, 3))
+    assert np.allclose(A.softmax_attention(q, k, ones, 1.0), 1.0, atol=1e-12)
+    v = rng.standard_normal((40, 5))
+    same_k = np.tile(k[:1], (40, 1))
+    assert np.allclose(A.softmax_attention(q, same_k, v, 1.0), v.mean(axis=0), atol=1e-12)
+
+
+def test_one_hot_row_returns_that_value_row():
+    k = np.eye(8)[:5] * 40.0
+    q = np.eye(8)[[2]]
+    v = np.arange(15.0).reshape(5, 3)
+    assert np.allclose(A.softmax_attention(q, k, v, 1.0), v[2], atol=1e-12)
+
+
+def _small_qkv(seed, B=1, N=200, M=30, H=2, D=64, spread=3.0):
+    rng = np.random.default_rng(seed)
+    mk = lambda n: (rng.standard_normal((B, n, H, D)) * rng.uniform(0.5, spread, (1, 1, H, 1))).astype(np.float32)
+    return mk(N), mk(N), mk(N), mk(M)
+
+
+def test_icl_attention_two_calls_share_keys_and_values():
+    qt, k, v, qe = _small_qkv(13)
+    o_tr, o_te = A.icl_attention(qt, k, v, qe, 0.125)
+    for h in range(2):
+        assert np.allclose(o_te[0, :, h], A.softmax_attention(qe[0, :, h], k[0, :, h], v[0, :, h], 0.125), atol=1e-13)
+        assert np.allclose(o_tr[0, :, h], A.softmax_attention(qt[0, :, h], k[0, :, h], v[0, :, h], 0.125), atol=1e-13)
+    # test queries equal to train queries give identical rows
+    o_tr2, o_te2 = A.icl_attention(qt, k, v, qt[:, :30], 0.125)
+    assert np.allclose(o_te2, o_tr2[:, :30], rtol=0, atol=1e-13)
+    # row selection (BLAS may block differently for different row counts)
+    s_tr, s_te = A.icl_attention(qt, k, v, qe, 0.125, rows_train=[5, 199], rows_test=[0, 29])
+    assert np.allclose(s_tr, o_tr[:, [5, 199]], rtol=0, atol=1e-13)
+    assert np.allclose(s_te, o_te[:, [0, 29]], rtol=0, atol=1e-13)
+
+
+@pytest.mark.parametrize("block_kv", [1, 16, 64, 77, 200, 4096])
+def test_kernel_model_without_p_rounding_equals_exact_attention(block_kv):
+    # With P kept exact, the one-pass online softmax must reproduce Eq. (1) on the
+    # dequantized inputs for any key-tile size (ragged tails included).
+    qt, k, v, qe = _small_qkv(14)
+    qz = Q.quantize_qkv_per_head(qt, k, v, qe)
+    ref_tr, ref_te = A.icl_attention_dequantized(qz, 0.125)
+    for row_sum in ("p8", "ptilde"):
+        o_tr, o_te = A.icl_attention_fp8_kernel_model(qz, 0.125, block_kv, quantize_p=False, row_sum=row_sum)
+        assert np.allclose(o_tr, ref_tr, rtol=1e-11, atol=1e-11 * np.abs(ref_tr).max())
+        assert np.allclose(o_te, ref_te, rtol=1e-11, atol=1e-11 * np.abs(ref_te).max())
+
+
+def p_rounding_bound(q, k, v, c):
+    """Elementwise bound on |O_qp - O_q| from the e4m3 rounding of P alone.
+
+    Each exact weight p_j = 2^(c(s_j - m) + 8) (m the final row max) is
+    replaced by a rounded one with |error| <= 2^-4 p_j (normal e4m3) or
+    <= 2^-10 (subnormal half step; later rescales only shrink it), and
+    O_qp - O_q = sum_j (w_j - p_j)(v_j - O_q) / sum_j w_j.
+    """
+    s = q @ k.T
+    p = np.exp2(c * (s - s.max(axis=1, keepdims=True)) + 8.0)
+    o = (p @ v) / p.sum(axis=1, keepdims=True)
+    e = 2.0 ** -4 * p + 2.0 ** -10
+    num = np.einsum("rj,rjc->rc", e, np.abs(v[None, :, :] - o[:, None, :]))
+    return o, num / (p.sum(axis=1) - e.sum(axis=1))[:, None]
+
+
+@pytest.mark.parametrize("block_kv,seed", [(64, 15), (32, 16), (500, 17)])
+def test_kernel_model_with_p_rounding_within_e4m3_bound(block_kv, seed):
+    qt, k, v, qe = _small_qkv(seed, N=300, M=20, spread=4.0)
+    qz = Q.quantize_qkv_per_head(qt, k, v, qe)
+    o_tr, o_te = A.icl_attention_fp8_kernel_model(qz, 0.125, block_kv)
+    ref_tr, ref_te = A.icl_attention_dequantized(qz, 0.125)
+    for h in range(2):
+        c = 0.125 * float(qz["s_q"][0, h]) * float(qz["s_k"][0, h]) * A.LOG2E
+        kq, vq = decode(qz["k8"][0, h]), decode(qz["v8"][0, h]) * float(qz["s_v"][0, h])
+        for q8, got, ref in ((qz["q8_train"], o_tr, ref_tr), (qz["q8_test"], o_te, ref_te)):
+            o, bnd = p_rounding_bound(decode(q8[0, h]), kq, vq, c)
+            assert np.allclose(o, ref[0, :, h], atol=1e-9 * np.abs(o).max())
+            err = np.abs(got[0, :, h] - ref[0, :, h])
+            assert np.all(err <= bnd * (1 + 1e-9) + 1e-12)
+            assert err.max() > 0                                      # P really is rounded
+
+
+def test_kernel_model_identical_keys_constant_v_and_one_hot():
+    rng = np.random.default_rng(18)
+    D, N = 64, 150
+    q8 = decode(encode_rne(np.clip(rng.standard_normal((10, D)) * 60, -448, 448)))
+    k8 = np.tile(decode(encode_rne(np.clip(rng.standard_normal((1, D)) * 60, -448, 448))), (N, 1))
+    v8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    # identical keys: every lifted weight is exactly 2^8, so the output is the mean of V exactly
+    o = A.one_pass_fp8_attention(q8, k8, v8, 0.01, 0.5, 64)
+    assert np.allclose(o, 0.5 * v8.mean(axis=0), rtol=0, atol=1e-12)
+    # constant V: the rounded weights are normalised by their own sum
+    k8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    vc = np.full((N, D), 3.5)
+    assert np.allclose(A.one_pass_fp8_attention(q8, k8, vc, 0.003, 2.0, 64), 7.0, rtol=0, atol=1e-12)
+    # one-hot: key 37 exceeds all others by > 20 in the base-2 logit, others round to 0
+    k8 = np.zeros((N, D)); k8[37, 0] = 448.0; q8 = np.zeros((1, D)); q8[0, 0] = 448.0
+    assert np.array_equal(A.one_pass_fp8_attention(q8, k8, v8, 1e-4, 1.0, 64)[0], v8[37])
+
+
+def test_kernel_model_lifts_row_max_to_256_and_weights_are_e4m3_values():
+    # V = identity reveals the normalised weights; with one key tile the largest weight is 2^8.
+    rng = np.random.default_rng(19)
+    N = D = 64
+    q8 = decode(encode_rne(np.clip(rng.standard_normal((5, D)) * 60, -448, 448)))
+    k8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    w = A.one_pass_fp8_attention(q8, k8, np.eye(N), 2e-4, 1.0, N)
+    p8 = 256.0 * w / w.max(axis=1, keepdims=True)
+    assert np.all(np.argmax(w, axis=1) == np.argmax(q8 @ k8.T, axis=1))
+    assert np.allclose(p8, decode(encode_rne(np.round(p8, 9))), rtol=0, atol=1e-9)
+
+
+def test_lift_keeps_subnormal_weights():
+    # Base-2 logits 0 and -17.5: with the 2^8 lift the small weight is 2^-9.5, which
+    # rounds to the smallest subnormal 2^-9 (a lift of 2^7 would round it to 0).
+    q8 = np.zeros((1, 64)); q8[0, 0] = 1.0
+    k8 = np.zeros((2, 64)); k8[0, 0] = 64.0; k8[1, 0] = 32.0
+    w = A.one_pass_fp8_attention(q8, k8, np.eye(2), 17.5 / 32.0, 1.0, 64)[0]
+    assert w[1] == 2.0 ** -9 / (256.0 + 2.0 ** -9)
+    assert w[0] == 256.0 / (256.0 + 2.0 ** -9)
