@@ -1,0 +1,208 @@
+#!/usr/bin/env python3
+"""FP8 ICL attention throughput on one MI355X, with the bf16 kernel beside it.
+
+One step is the whole hot path on one batch: per-head absmax quantization of
+Q_train, K, V and Q_test to e4m3 (Eq. (2)), then both ICL attention calls
+(train-train and test-train, Sec. 3) in FP8, i.e. one tfm_icl_attention_fp8
+call, timed as its two stages with HIP events on the stream the library
+launches on.  Inputs are resident in HBM before timing starts.  The headline
+workload is two independent tables with 65536 train and 16384 test rows,
+6 heads of dimension 64, bf16 in and out.  FLOPs count QK^T and PV of both
+calls: 4*B*H*D*N*(N+M).
+
+Prints one JSON line on stdout; progress goes to stderr.
+"""
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "FP8 ICL attention TFLOP/s + speedup vs bf16 at N_train=65536, 1 MI355X"
+FP8_PEAK_TFLOPS = 5000.0          # MI355X dense FP8 MFMA
+COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
+ATTN_SRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc", "attn_fp8.hip")
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def source_digest():
+    with open(ATTN_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def traffic_from_counters(n_dispatch_units):
+    """HBM bytes per attention launch from the committed rocprofv3 --pmc summary,
+    or None when it is missing or was taken on a different attn_fp8.hip."""
+    if not os.path.exists(COUNTERS):
+        return None
+    kv = {}
+    for line in open(COUNTERS):
+        if ":" in line and not line.startswith("#"):
+            k, v = line.split(":", 1)
+            kv[k.strip()] = v.strip()
+    if kv.get("attn_fp8_source_sha256_16") != source_digest():
+        return None
+    try:
+        return float(kv["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(x, w, rows):
+    """The oracle, single-threaded, on a bounded sample of the same workload."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    from oracle import attention as OA
+    from oracle import quantize as OQ
+
+    with threadpool_limits(limits=1):
+        sl = lambda a: np.ascontiguousarray(a[:1, :, :1, :])          # table 0, head 0
+        t0 = time.perf_counter()
+        qz = OQ.quantize_qkv_per_head(sl(x["q_train"]), sl(x["k"]), sl(x["v"]), sl(x["q_test"]))
+        t_quant = time.perf_counter() - t0
+        t0 = time.perf_counter()
+        OA.icl_attention_fp8_kernel_model(qz, w.alpha, 64, np.arange(rows), [])
+        t_attn = time.perf_counter() - t0
+    flops = 4.0 * w.D * w.N * rows
+    return {"value": flops / t_attn / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
+            "sample": "one-pass FP8 kernel model (fp64 numpy) for %d train query rows of table 0, head 0, "
+                      "against all %d keys; quantization of that head (N+M rows) took %.2f s more" %
+                      (rows, w.N, t_quant),
+            "seconds": round(t_attn, 2)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mid")
+    ap.add_argument("--cpu-rows", type=int, default=1024, help="query rows of the oracle sample")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-bf16", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also run a 1 GiB device copy (for scaling HBM counters)")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print("bench.py measures one GPU only: the FP8 ICL attention of each (table, head) is independent, "
+              "and multi-GPU runs are not part of this build (asked for --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2609_13031_amd import tfm
+    from paper_2609_13031_amd.workloads import WORKLOADS, generate
+
+    tfm.lib()
+    w = WORKLOADS[args.workload]
+    log("generating", w)
+    x = generate(w)
+    in_dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
+    dev = torch.device("cuda:0")
+    g = {k: torch.from_numpy(v).to(in_dt).to(dev) for k, v in x.items()}
+    out_dt = torch.bfloat16
+    o_tr = torch.empty((w.B, w.N, w.H, w.D), dtype=out_dt, device=dev)
+    o_te = torch.empty((w.B, w.M, w.H, w.D), dtype=out_dt, device=dev)
+    ws = torch.empty(tfm.tfm_icl_attention_fp8_workspace_bytes(w.B, w.H, w.D, w.N, w.M), dtype=torch.uint8,
+                     device=dev)
+
+    def quantize():
+        tfm.tfm_icl_attention_fp8_quantize(g["q_train"], g["k"], g["v"], g["q_test"], workspace=ws)
+
+    def attend():
+        tfm.tfm_icl_attention_fp8_attend(ws, w.B, w.H, w.D, w.N, w.M, alpha=w.alpha, out_dtype=out_dt,
+                                         out=(o_tr, o_te))
+
+    log("warmup", args.warmup)
+    for _ in range(args.warmup):
+        quantize()
+        attend()
+    torch.cuda.synchronize()
+
+    K = args.steps
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(K)]
+    begin, end = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_wall = time.perf_counter()
+    begin.record()
+    for i in range(K):
+        ev[i][0].record()
+        quantize()
+        ev[i][1].record()
+        attend()
+        ev[i][2].record()
+    end.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - t_wall) * 1e3
+    total_ms = begin.elapsed_time(end)
+    ms_step = total_ms / K
+    q_ms = [e[0].elapsed_time(e[1]) for e in ev]
+    a_ms = [e[1].elapsed_time(e[2]) for e in ev]
+    attn_ms = sum(a_ms) / K
+    quant_ms = sum(q_ms) / K
+    log("fp8 step %.3f ms (quantize %.3f, attention %.3f), wall %.1f ms for %d steps" %
+        (ms_step, quant_ms, attn_ms, wall_ms, K))
+
+    bf16 = None
+    if not args.no_bf16:
+        gb = g if in_dt == torch.bfloat16 else {k: v.to(torch.bfloat16) for k, v in g.items()}
+        b_tr, b_te = torch.empty_like(o_tr), torch.empty_like(o_te)
+        run_bf16 = lambda: tfm.tfm_icl_attention_bf16(gb["q_train"], gb["k"], gb["v"], gb["q_test"], alpha=w.alpha,
+                                                      out_dtype=out_dt, out=(b_tr, b_te))
+        for _ in range(args.warmup):
+            run_bf16()
+        torch.cuda.synchronize()
+        b0, b1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        b0.record()
+        for _ in range(K):
+            run_bf16()
+        b1.record()
+        torch.cuda.synchronize()
+        bf16_ms = b0.elapsed_time(b1) / K
+        bf16 = {"ms": round(bf16_ms, 4), "tflops": round(w.flops / bf16_ms / 1e9, 2)}
+        log("bf16 %.3f ms" % bf16_ms)
+
+    if args.copy_calibration:
+        a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        for _ in range(3):
+            b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy calibration: 3 x 1 GiB device copies done")
+
+    value = w.flops / ms_step / 1e9                      # TFLOP/s
+    achieved = w.flops / attn_ms / 1e9
+    traffic = traffic_from_counters(1)
+    result = {
+        "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "fp8_e4m3", "data": "synthetic",
+        "config": {"workload": "%s: B=%d tables, H=%d heads, D=%d, N_train=%d, N_test=%d, %s in, bf16 out"
+                               % (w.name, w.B, w.H, w.D, w.N, w.M, w.dtype),
+                   "B": w.B, "H": w.H, "D": w.D, "N_train": w.N, "N_test": w.M, "in_dtype": w.dtype,
+                   "out_dtype": "bf16", "parallelism": "single GPU"},
+        "stages_ms": {"quantize": round(quant_ms, 4), "attention": round(attn_ms, 4)},
+        "speedup_vs_bf16": round(bf16["ms"] / ms_step, 3) if bf16 else None,
+        "attention_only_speedup_vs_bf16": round(bf16["ms"] / attn_ms, 3) if bf16 else None,
+        "bf16": bf16,
+        "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
+                     "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
+                     "traffic": traffic},
+    }
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) on %d rows" % args.cpu_rows)
+        result["cpu_baseline"] = cpu_baseline(x, w, args.cpu_rows)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

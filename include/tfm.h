@@ -1,0 +1,187 @@
+/*
+ * tfm.h -- C ABI of libtfm: FP8 in-context-learning (ICL) attention for
+ * tabular foundation models on AMD Instinct MI355X (gfx950).
+ *
+ * The operation is the one of "Attention Quantization for Tabular Foundation
+ * Models" (Sec. 3, Method):
+ *   - Eq. (1): Attn(Q,K,V) = P V with P = softmax(alpha Q K^T), row-wise;
+ *   - the ICL layer evaluates it twice per head, train-train (N train queries
+ *     against the N train keys) and test-train (M test queries against the
+ *     same N train keys and values);
+ *   - Eq. (2): every tensor is quantized per head to OCP e4m3fn with a
+ *     dynamic absmax scale s = max|X| / 448 and X_8 = rn(clamp(X/s, +-448));
+ *     test queries reuse the scale of the train queries (batch invariance);
+ *   - inside the fused kernel (Fig. 2): the Q and K scales are applied
+ *     together with the softmax scale, P is lifted so that its row maximum is
+ *     2^8 and rounded to e4m3, and the V scale is applied in the epilogue.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - B tables, H heads, D head_dim (64 or 128), N train rows (>= 1), M test
+ *    rows (>= 0).  Activations are row-major (B, rows, H, D), the layout the
+ *    paper writes as X in R^{S x H x d}; quantized codes are row-major
+ *    (B, H, rows, D) uint8; scales are (B, H) float32 dequantization scales.
+ *  - All tensor pointers are device memory owned by the caller and borrowed
+ *    for the call; they must be 16-byte aligned and must not alias each
+ *    other.  A pointer whose element count is 0 (q_test / o_test / q8_test
+ *    when M == 0) may be NULL.  The library never allocates device memory
+ *    and keeps no state between calls, so calls are thread-safe.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *    null stream); no entry point synchronizes.
+ *  - Every argument is validated before anything is enqueued; on error
+ *    nothing is enqueued and a tfm_status other than TFM_OK is returned.
+ *    TFM_ERR_HIP means the HIP runtime refused a launch.  No C++ exception
+ *    crosses this interface.
+ *  - Inputs must be finite; for non-finite inputs the results are
+ *    unspecified.
+ */
+#ifndef TFM_H_
+#define TFM_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  TFM_OK = 0,
+  TFM_ERR_NULL_PTR = 1,             /* a required pointer is NULL */
+  TFM_ERR_BAD_SHAPE = 2,            /* B, H < 1, N < 1, M < 0, or a size overflows */
+  TFM_ERR_BAD_DTYPE = 3,            /* dtype code not accepted by this entry point */
+  TFM_ERR_UNSUPPORTED_HEAD_DIM = 4, /* D is not 64 or 128 */
+  TFM_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
+  TFM_ERR_WORKSPACE_TOO_SMALL = 6,  /* workspace_bytes below the size query */
+  TFM_ERR_HIP = 7,                  /* the HIP runtime reported an error */
+  TFM_ERR_BAD_ARG = 8               /* alpha is not finite and positive */
+} tfm_status;
+
+typedef enum { TFM_F32 = 0, TFM_BF16 = 1 } tfm_dtype;
+
+/* A hipStream_t, passed as an opaque pointer. */
+typedef void* tfm_stream;
+
+/* Human-readable name of a status code (static storage, never NULL). */
+const char* tfm_status_string(int status);
+
+/* Library version as major*10000 + minor*100 + patch. */
+int tfm_version(void);
+
+/*
+ * tfm_quantize_qkv_per_head -- Eq. (2) for the ICL layer (Sec. 3).
+ *
+ * For every (b, h): s_q = fl32(max|Q_train| / 448), s_k and s_v likewise
+ * (fp32 division; a head whose scale would be 0 gets scale 1), and each
+ * element becomes the e4m3fn code of clamp(fl32(x / s), -448, 448), rounded
+ * to nearest, ties to even.  Q_test is quantized with s_q of Q_train.
+ *
+ *   in_dtype            TFM_F32 or TFM_BF16, the element type of the inputs
+ *   q_train, k, v       (B, N, H, D) inputs
+ *   q_test              (B, M, H, D) input, NULL iff M == 0
+ *   q8_train, k8, v8    (B, H, N, D) uint8 outputs
+ *   q8_test             (B, H, M, D) uint8 output, NULL iff M == 0
+ *   s_q, s_k, s_v       (B, H) float32 outputs
+ *   workspace           >= tfm_quantize_workspace_bytes(B, H) device bytes
+ *                       of scratch (contents on entry are ignored)
+ */
+size_t tfm_quantize_workspace_bytes(int B, int H);
+int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M,
+                              const void* q_train, const void* k, const void* v,
+                              const void* q_test, uint8_t* q8_train, uint8_t* k8,
+                              uint8_t* v8, uint8_t* q8_test, float* s_q, float* s_k,
+                              float* s_v, void* workspace, size_t workspace_bytes,
+                              tfm_stream stream);
+
+/*
+ * tfm_icl_attention_fp8 -- the full hot path: Eq. (2) quantization of
+ * Q_train, K, V and Q_test (test queries on the train-query scale), then
+ * both ICL attention calls of Sec. 3 in one fused FP8 launch over the N + M
+ * query rows, against the same quantized keys and values.
+ *
+ * Per (b, h) and query row i, over key tiles of tfm_icl_attention_fp8_block_kv(D)
+ * keys in order: S = Q_8 K_8^T (FP8 products, fp32 accumulation); running
+ * max m; P~ = 2^(c (S - m) + 8) with c = alpha * s_q * s_k * log2(e), so the
+ * running row maximum maps to 2^8 (Sec. 3, the P paragraph); P_8 = e4m3(P~)
+ * rounded to nearest even; l and O = sum P_8 V_8 are rescaled by
+ * 2^(c (m_old - m)) when m grows; the epilogue writes O * s_v / l.  The row
+ * sum l accumulates the rounded P_8.
+ *
+ *   in_dtype            TFM_F32 or TFM_BF16 (inputs)
+ *   out_dtype           TFM_F32 or TFM_BF16 (outputs)
+ *   alpha               softmax scale (finite, > 0), usually 1/sqrt(D)
+ *   q_train, k, v       (B, N, H, D);  q_test (B, M, H, D), NULL iff M == 0
+ *   o_train             (B, N, H, D) output;  o_test (B, M, H, D), NULL iff M == 0
+ *   workspace           >= tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
+ *                       device bytes of scratch (contents on entry ignored);
+ *                       it holds the codes and scales of the call
+ */
+size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M);
+int tfm_icl_attention_fp8(int in_dtype, int out_dtype, int B, int H, int D, int N, int M,
+                          float alpha, const void* q_train, const void* k, const void* v,
+                          const void* q_test, void* o_train, void* o_test, void* workspace,
+                          size_t workspace_bytes, tfm_stream stream);
+
+/*
+ * The two stages of tfm_icl_attention_fp8, which is exactly
+ * tfm_icl_attention_fp8_quantize followed by tfm_icl_attention_fp8_attend on
+ * the same workspace: for callers that time the stages or run the attention
+ * again on codes that are already in the workspace.
+ *
+ * tfm_icl_attention_fp8_quantize -- Eq. (2) for Q_train, K, V and Q_test
+ *   (on the train-query scale) into `workspace`, in the private layout the
+ *   attention stage reads (arguments as for tfm_icl_attention_fp8).
+ * tfm_icl_attention_fp8_attend -- both ICL calls from a workspace filled by
+ *   tfm_icl_attention_fp8_quantize with the same B, H, D, N, M; the
+ *   workspace is only read.  Outputs as for tfm_icl_attention_fp8.
+ */
+int tfm_icl_attention_fp8_quantize(int in_dtype, int B, int H, int D, int N, int M,
+                                   const void* q_train, const void* k, const void* v,
+                                   const void* q_test, void* workspace, size_t workspace_bytes,
+                                   tfm_stream stream);
+int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                                 void* o_train, void* o_test, const void* workspace,
+                                 size_t workspace_bytes, tfm_stream stream);
+
+/*
+ * tfm_icl_attention_fp8_prequantized -- the attention part of
+ * tfm_icl_attention_fp8 on codes and scales produced by
+ * tfm_quantize_qkv_per_head (same layouts), e.g. to reuse K_8 / V_8 for
+ * several test batches.  The workspace receives a re-laid-out copy of V_8.
+ *
+ *   q8_train, k8, v8    (B, H, N, D) uint8;  q8_test (B, H, M, D), NULL iff M == 0
+ *   s_q, s_k, s_v       (B, H) float32
+ *   workspace           >= tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
+ */
+size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, int N);
+int tfm_icl_attention_fp8_prequantized(int out_dtype, int B, int H, int D, int N, int M,
+                                       float alpha, const uint8_t* q8_train,
+                                       const uint8_t* k8, const uint8_t* v8,
+                                       const uint8_t* q8_test, const float* s_q,
+                                       const float* s_k, const float* s_v, void* o_train,
+                                       void* o_test, void* workspace, size_t workspace_bytes,
+                                       tfm_stream stream);
+
+/* Number of keys per tile of the FP8 kernel for head_dim D (the granularity
+ * of its running maximum); 0 for an unsupported D. */
+int tfm_icl_attention_fp8_block_kv(int D);
+
+/*
+ * tfm_icl_attention_bf16 -- the 16-bit baseline of the same two ICL calls
+ * (Eq. (1), no quantization): bf16 Q/K/V, fp32 online softmax in one pass,
+ * P rounded to bf16 for the PV product, fp32 accumulation.
+ *
+ *   q_train, k, v       (B, N, H, D) bf16;  q_test (B, M, H, D) bf16, NULL iff M == 0
+ *   out_dtype           TFM_F32 or TFM_BF16
+ *   o_train, o_test     as for tfm_icl_attention_fp8
+ */
+int tfm_icl_attention_bf16(int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                           const void* q_train, const void* k, const void* v,
+                           const void* q_test, void* o_train, void* o_test,
+                           tfm_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TFM_H_ */

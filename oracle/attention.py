@@ -89,18 +89,27 @@ def icl_attention_dequantized(qz, alpha, rows_train=None, rows_test=None):
                          q_te, alpha, rows_train, rows_test)
 
 
-def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_sum="p8"):
+def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_sum="p8", tie_rel=None):
     """One head of the fused FP8 kernel, replayed in fp64.
 
     q8 (R,D), k8 (N,D), v8 (N,D) are the e4m3 *values* (decoded codes),
     c = alpha * s_q * s_k * log2(e) is the factor that turns a raw code dot
     product into a base-2 logit, s_v the V dequantization scale.
+
+    With ``tie_rel`` set, also returns the sensitivity of the result to
+    rounding ties of P: for every P~ whose e4m3 rounding changes when P~ moves
+    by a relative tie_rel, the two candidate codes differ by ``spread``; if an
+    implementation picks the other one for any such keys, its output moves by
+    at most sum_j spread_j r_j (|v_j| + |o|) / l (r_j the later rescales), which
+    is returned elementwise as (o, allowance).
     """
     R, D = q8.shape
     N = k8.shape[0]
     m = np.full(R, -np.inf)
     l = np.zeros(R)
     acc = np.zeros((R, v8.shape[1]))
+    tie_l = np.zeros(R)
+    tie_acc = np.zeros((R, v8.shape[1]))
     for j0 in range(0, N, block_kv):
         s = q8 @ k8[j0:j0 + block_kv].T          # exact: products of e4m3 values
         m_new = np.maximum(m, s.max(axis=1))
@@ -109,16 +118,24 @@ def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_su
         r = np.exp2(c * (m - m_new))             # rescale of the old state; 0 at the start
         l = l * r + (p8 if row_sum == "p8" else p).sum(axis=1)
         acc = acc * r[:, None] + p8 @ v8[j0:j0 + block_kv]
+        if tie_rel is not None:
+            spread = round_to_e4m3(p * (1 + tie_rel)) - round_to_e4m3(p * (1 - tie_rel))
+            tie_l = tie_l * r + spread.sum(axis=1)
+            tie_acc = tie_acc * r[:, None] + spread @ np.abs(v8[j0:j0 + block_kv])
         m = m_new
-    return acc * float(s_v) / l[:, None]
+    o = acc * float(s_v) / l[:, None]
+    if tie_rel is None:
+        return o
+    return o, (tie_acc * float(s_v) + tie_l[:, None] * np.abs(o)) / l[:, None]
 
 
 def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_test=None,
-                                   quantize_p=True, row_sum="p8"):
+                                   quantize_p=True, row_sum="p8", tie_rel=None):
     """O_qp: both ICL calls through ``one_pass_fp8_attention`` for every (b, h).
 
     ``qz`` is the output of ``quantize_qkv_per_head``.  Returns (o_train,
-    o_test) as (B, R, H, D) fp64 for the selected rows.
+    o_test) as (B, R, H, D) fp64 for the selected rows; with ``tie_rel`` set,
+    returns ((o_train, allowance_train), (o_test, allowance_test)).
     """
     B, H, N, D = qz["k8"].shape
     rt = _pick(rows_train, N)
@@ -126,13 +143,22 @@ def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_te
     re = _pick(rows_test, M)
     o_tr = np.zeros((B, len(rt), H, D))
     o_te = np.zeros((B, len(re), H, D))
+    a_tr = np.zeros_like(o_tr)
+    a_te = np.zeros_like(o_te)
     for b in range(B):
         for h in range(H):
             c = float(alpha) * float(qz["s_q"][b, h]) * float(qz["s_k"][b, h]) * LOG2E
             kq = decode(qz["k8"][b, h])
             vq = decode(qz["v8"][b, h])
-            args = (kq, vq, c, qz["s_v"][b, h], block_kv, quantize_p, row_sum)
-            o_tr[b, :, h] = one_pass_fp8_attention(decode(qz["q8_train"][b, h, rt]), *args)
-            if len(re):
-                o_te[b, :, h] = one_pass_fp8_attention(decode(qz["q8_test"][b, h, re]), *args)
-    return o_tr, o_te
+            args = (kq, vq, c, qz["s_v"][b, h], block_kv, quantize_p, row_sum, tie_rel)
+            for o, a, key, rows in ((o_tr, a_tr, "q8_train", rt), (o_te, a_te, "q8_test", re)):
+                if len(rows) == 0:
+                    continue
+                res = one_pass_fp8_attention(decode(qz[key][b, h, rows]), *args)
+                if tie_rel is None:
+                    o[b, :, h] = res
+                else:
+                    o[b, :, h], a[b, :, h] = res
+    if tie_rel is None:
+        return o_tr, o_te
+    return (o_tr, a_tr), (o_te, a_te)

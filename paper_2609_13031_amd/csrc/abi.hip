@@ -1,0 +1,225 @@
+// libtfm C ABI: argument validation, workspace layout and launch sequences.
+// The operations and conventions are documented in include/tfm.h.
+#include <climits>
+#include <cmath>
+
+#include "../../include/tfm.h"
+#include "common.h"
+
+namespace tfm {
+
+static size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t v8t_bytes(int B, int H, int D, int N) {
+  return (size_t)B * H * (size_t)((N + 63) / 64) * 64 * D;
+}
+
+Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M) {
+  Fp8Workspace w;
+  const size_t bh = (size_t)B * H;
+  size_t off = 0;
+  w.amax = off;      off += align256(3 * bh * sizeof(uint32_t));
+  w.scales = off;    off += align256(3 * bh * sizeof(float));
+  w.q8_train = off;  off += align256(bh * N * D);
+  w.q8_test = off;   off += align256(bh * (size_t)M * D);
+  w.k8 = off;        off += align256(bh * N * D);
+  w.v8t = off;       off += align256(v8t_bytes(B, H, D, N));
+  w.total = off;
+  return w;
+}
+
+}  // namespace tfm
+
+namespace {
+
+using namespace tfm;
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Shapes every entry point accepts.  Limits: B*H <= 65535 (a grid dimension),
+// N + M below INT_MAX - 256 (row indices are 32-bit), B*H*ceil((N+M)/128)
+// workgroups at most INT_MAX, and B*H*D*(N+M) elements at most 2^48.
+int check_shape(int B, int H, int D, int N, int M) {
+  if (B < 1 || H < 1 || N < 1 || M < 0) return TFM_ERR_BAD_SHAPE;
+  if ((long long)B * H > 65535) return TFM_ERR_BAD_SHAPE;
+  if ((long long)N + M > (long long)INT_MAX - 256) return TFM_ERR_BAD_SHAPE;
+  if (D != 64 && D != 128) return TFM_ERR_UNSUPPORTED_HEAD_DIM;
+  if (((long long)N + M + 127) / 128 * B * H > (long long)INT_MAX) return TFM_ERR_BAD_SHAPE;  // attention grid
+  const long double elems = (long double)B * H * D * ((long double)N + M);
+  if (elems > 281474976710656.0L) return TFM_ERR_BAD_SHAPE;
+  return TFM_OK;
+}
+
+int check_io(bool need_test, const void* const* req, int nreq, const void* const* test_ptrs, int ntest) {
+  for (int i = 0; i < nreq; ++i) if (!req[i]) return TFM_ERR_NULL_PTR;
+  if (need_test) for (int i = 0; i < ntest; ++i) if (!test_ptrs[i]) return TFM_ERR_NULL_PTR;
+  for (int i = 0; i < nreq; ++i) if (!aligned16(req[i])) return TFM_ERR_MISALIGNED;
+  for (int i = 0; i < ntest; ++i) if (test_ptrs[i] && !aligned16(test_ptrs[i])) return TFM_ERR_MISALIGNED;
+  return TFM_OK;
+}
+
+int check_alpha(float alpha) { return (std::isfinite(alpha) && alpha > 0.0f) ? TFM_OK : TFM_ERR_BAD_ARG; }
+
+int hip_status(hipError_t e) { return e == hipSuccess ? TFM_OK : TFM_ERR_HIP; }
+
+#define TFM_TRY(expr) do { int st_ = (expr); if (st_ != TFM_OK) return st_; } while (0)
+#define TFM_HIP(expr) do { if ((expr) != hipSuccess) return TFM_ERR_HIP; } while (0)
+
+// amax + scales + the four code tensors.  v8 == nullptr writes V to v8t instead.
+int quantize_all(int in_dtype, int B, int H, int D, int N, int M, const void* q_train, const void* k,
+                 const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8, uint8_t* v8t,
+                 uint8_t* q8_test, uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
+                 hipStream_t s) {
+  const int bf = in_dtype == TFM_BF16;
+  const int BH = B * H;
+  TFM_HIP(launch_fill_zero_u32(amax, 3 * BH, s));
+  TFM_HIP(launch_amax(bf, B, H, D, N, q_train, k, v, amax, s));
+  TFM_HIP(launch_scales(BH, amax, scales, s_q, s_k, s_v, s));
+  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, q_train, scales, q8_train, s));
+  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales, q8_test, s));
+  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, k, scales + BH, k8, s));
+  if (v8) TFM_HIP(launch_quantize_rows(bf, B, H, D, N, v, scales + 2 * BH, v8, s));
+  else TFM_HIP(launch_quantize_v_tiles(bf, B, H, D, N, v, scales + 2 * BH, v8t, s));
+  return TFM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* tfm_status_string(int status) {
+  switch (status) {
+    case TFM_OK: return "TFM_OK";
+    case TFM_ERR_NULL_PTR: return "TFM_ERR_NULL_PTR: a required pointer is NULL";
+    case TFM_ERR_BAD_SHAPE: return "TFM_ERR_BAD_SHAPE: B, H >= 1, N >= 1, M >= 0 and sizes within limits required";
+    case TFM_ERR_BAD_DTYPE: return "TFM_ERR_BAD_DTYPE: unsupported dtype code";
+    case TFM_ERR_UNSUPPORTED_HEAD_DIM: return "TFM_ERR_UNSUPPORTED_HEAD_DIM: D must be 64 or 128";
+    case TFM_ERR_MISALIGNED: return "TFM_ERR_MISALIGNED: pointers must be 16-byte aligned";
+    case TFM_ERR_WORKSPACE_TOO_SMALL: return "TFM_ERR_WORKSPACE_TOO_SMALL: workspace below the size query";
+    case TFM_ERR_HIP: return "TFM_ERR_HIP: the HIP runtime reported an error";
+    case TFM_ERR_BAD_ARG: return "TFM_ERR_BAD_ARG: alpha must be finite and positive";
+    default: return "TFM_ERR_UNKNOWN";
+  }
+}
+
+int tfm_version(void) { return 100; }
+
+size_t tfm_quantize_workspace_bytes(int B, int H) {
+  if (B < 1 || H < 1) return 0;
+  return align256(3 * (size_t)B * H * sizeof(uint32_t)) + align256(3 * (size_t)B * H * sizeof(float));
+}
+
+int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M, const void* q_train, const void* k,
+                              const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8,
+                              uint8_t* q8_test, float* s_q, float* s_k, float* s_v, void* workspace,
+                              size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  const void* req[] = {q_train, k, v, q8_train, k8, v8, s_q, s_k, s_v, workspace};
+  const void* tst[] = {q_test, q8_test};
+  TFM_TRY(check_io(M > 0, req, 10, tst, 2));
+  if (workspace_bytes < tfm_quantize_workspace_bytes(B, H)) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* ws = (uint8_t*)workspace;
+  uint32_t* amax = (uint32_t*)ws;
+  float* scales = (float*)(ws + align256(3 * (size_t)B * H * sizeof(uint32_t)));
+  return quantize_all(in_dtype, B, H, D, N, M, q_train, k, v, q_test, q8_train, k8, v8, nullptr, q8_test, amax,
+                      scales, s_q, s_k, s_v, (hipStream_t)stream);
+}
+
+size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M) {
+  if (check_shape(B, H, D, N, M) != TFM_OK) return 0;
+  return fp8_workspace_layout(B, H, D, N, M).total;
+}
+
+int tfm_icl_attention_fp8_quantize(int in_dtype, int B, int H, int D, int N, int M, const void* q_train,
+                                   const void* k, const void* v, const void* q_test, void* workspace,
+                                   size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  const void* req[] = {q_train, k, v, workspace};
+  const void* tst[] = {q_test};
+  TFM_TRY(check_io(M > 0, req, 4, tst, 1));
+  const Fp8Workspace L = fp8_workspace_layout(B, H, D, N, M);
+  if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* ws = (uint8_t*)workspace;
+  return quantize_all(in_dtype, B, H, D, N, M, q_train, k, v, q_test, ws + L.q8_train, ws + L.k8, nullptr,
+                      ws + L.v8t, ws + L.q8_test, (uint32_t*)(ws + L.amax), (float*)(ws + L.scales), nullptr,
+                      nullptr, nullptr, (hipStream_t)stream);
+}
+
+int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int M, float alpha, void* o_train,
+                                 void* o_test, const void* workspace, size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  const void* req[] = {o_train, workspace};
+  const void* tst[] = {o_test};
+  TFM_TRY(check_io(M > 0, req, 2, tst, 1));
+  const Fp8Workspace L = fp8_workspace_layout(B, H, D, N, M);
+  if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  const uint8_t* ws = (const uint8_t*)workspace;
+  const float* scales = (const float*)(ws + L.scales);
+  const int BH = B * H;
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, alpha, ws + L.q8_train, ws + L.q8_test,
+                                    ws + L.k8, ws + L.v8t, scales, scales + BH, scales + 2 * BH, o_train, o_test,
+                                    (hipStream_t)stream));
+}
+
+int tfm_icl_attention_fp8(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                          const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
+                          void* o_test, void* workspace, size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  const void* req[] = {q_train, k, v, o_train, workspace};
+  const void* tst[] = {q_test, o_test};
+  TFM_TRY(check_io(M > 0, req, 5, tst, 2));
+  if (workspace_bytes < fp8_workspace_layout(B, H, D, N, M).total) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  TFM_TRY(tfm_icl_attention_fp8_quantize(in_dtype, B, H, D, N, M, q_train, k, v, q_test, workspace, workspace_bytes,
+                                         stream));
+  return tfm_icl_attention_fp8_attend(out_dtype, B, H, D, N, M, alpha, o_train, o_test, workspace, workspace_bytes,
+                                      stream);
+}
+
+size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, int N) {
+  if (check_shape(B, H, D, N, 0) != TFM_OK) return 0;
+  return align256(v8t_bytes(B, H, D, N));
+}
+
+int tfm_icl_attention_fp8_prequantized(int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                                       const uint8_t* q8_train, const uint8_t* k8, const uint8_t* v8,
+                                       const uint8_t* q8_test, const float* s_q, const float* s_k,
+                                       const float* s_v, void* o_train, void* o_test, void* workspace,
+                                       size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  const void* req[] = {q8_train, k8, v8, s_q, s_k, s_v, o_train, workspace};
+  const void* tst[] = {q8_test, o_test};
+  TFM_TRY(check_io(M > 0, req, 8, tst, 2));
+  if (workspace_bytes < tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N))
+    return TFM_ERR_WORKSPACE_TOO_SMALL;
+  hipStream_t s = (hipStream_t)stream;
+  uint8_t* v8t = (uint8_t*)workspace;
+  TFM_HIP(launch_relayout_v_tiles(B, H, D, N, v8, v8t, s));
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, alpha, q8_train, q8_test, k8, v8t,
+                                    s_q, s_k, s_v, o_train, o_test, s));
+}
+
+int tfm_icl_attention_fp8_block_kv(int D) { return (D == 64 || D == 128) ? kBlockKv : 0; }
+
+int tfm_icl_attention_bf16(int out_dtype, int B, int H, int D, int N, int M, float alpha, const void* q_train,
+                           const void* k, const void* v, const void* q_test, void* o_train, void* o_test,
+                           tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  const void* req[] = {q_train, k, v, o_train};
+  const void* tst[] = {q_test, o_test};
+  TFM_TRY(check_io(M > 0, req, 4, tst, 2));
+  return hip_status(launch_attn_bf16(out_dtype == TFM_BF16, B, H, D, N, M, alpha, q_train, q_test, k, v, o_train,
+                                     o_test, (hipStream_t)stream));
+}
+
+}  // extern "C"

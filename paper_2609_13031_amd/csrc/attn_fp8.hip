@@ -1,0 +1,222 @@
+// Fused FP8 ICL attention on gfx950 (train-train and test-train in one launch).
+//
+// The kernel of Sec. 3 / Fig. 2 of the paper, laid out for CDNA4:
+//  * a workgroup of 4 wave64s owns 128 consecutive query rows of one (b, h)
+//    out of the N train + M test rows (both ICL calls share K_8 and V_8, so
+//    they are one launch); each wave owns 32 rows;
+//  * key tiles of 64 are staged through LDS; per tile each wave computes
+//    S^T = K_8 Q_8^T with two v_mfma_f32_32x32x64_f8f6f4 per 64 of head_dim
+//    (fp32 accumulation), so every lane holds 32 scores of one query row;
+//  * online softmax in the exp2 domain: running max m, P~ = 2^(c S + 8 - c m)
+//    with c = alpha * s_q * s_k * log2(e) (the Q and K scales applied with the
+//    softmax scale), so the running row maximum maps to 2^8; P~ is rounded
+//    to e4m3 by v_cvt_pk_fp8_f32 (round to nearest even);
+//  * the e4m3 P tile of the QK^T accumulator is directly the B operand of
+//    O^T += V_8^T P_8^T (v_mfma_f32_32x32x64_f8f6f4): V is stored
+//    tile-transposed with its keys in the accumulator's row order, so no
+//    shuffle is needed;
+//  * the row sum l = sum P_8 comes from one v_mfma_f32_16x16x128_f8f6f4 of a
+//    constant 0/1 operand against the same P_8 operand;
+//  * epilogue: O * s_v / l (the V scale applied last), fp32 or bf16 out.
+#include "common.h"
+
+namespace tfm {
+namespace {
+
+constexpr int kWaves = 4;
+constexpr int kRowsPerWave = 32;
+constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
+constexpr int kPad = 16;  // LDS row padding (bytes): conflict-free 16-byte lane reads
+
+struct Fp8Args {
+  int B, H, N, M, tiles;
+  float alpha;
+  const uint8_t* q8_train;
+  const uint8_t* q8_test;
+  const uint8_t* k8;
+  const uint8_t* v8t;
+  const float* s_q;
+  const float* s_k;
+  const float* s_v;
+  void* o_train;
+  void* o_test;
+};
+
+__device__ inline v8i load32(const uint8_t* p) {
+  u32x4 a = *reinterpret_cast<const u32x4*>(p);
+  u32x4 b = *reinterpret_cast<const u32x4*>(p + 16);
+  return v8i{(int)a.x, (int)a.y, (int)a.z, (int)a.w, (int)b.x, (int)b.y, (int)b.z, (int)b.w};
+}
+
+__device__ inline v16f mfma_f8_32x32x64(v8i a, v8i b, v16f c) {
+  return __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+__device__ inline v4f mfma_f8_16x16x128(v8i a, v8i b, v4f c) {
+  return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
+}
+
+template <int D, bool OUT_BF16>
+__global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
+  constexpr int KD = D / 64;            // 64-wide head_dim chunks (k of one MFMA)
+  constexpr int KS = D + kPad;          // K tile row stride in LDS
+  constexpr int VS = 64 + kPad;         // V^T tile row stride in LDS
+  __shared__ __attribute__((aligned(16))) uint8_t k_lds[64 * KS];
+  __shared__ __attribute__((aligned(16))) uint8_t v_lds[D * VS];
+
+  const int bh = blockIdx.x / a.tiles;
+  const int tile = blockIdx.x % a.tiles;
+  const int b = bh / a.H, h = bh % a.H;
+  const int N = a.N, M = a.M;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+  const int ql = lane % 32, half = lane / 32;
+  const int row = tile * kRowsPerBlock + wave * kRowsPerWave + ql;   // in [0, N+M)
+
+  // Q_8 fragment: lane holds head_dim bytes [64s + 32*half, +32) of its row
+  v8i qf[KD];
+  {
+    const uint8_t* qrow = nullptr;
+    if (row < N) qrow = a.q8_train + ((size_t)bh * N + row) * D;
+    else if (row < N + M) qrow = a.q8_test + ((size_t)bh * M + (row - N)) * D;
+#pragma unroll
+    for (int s = 0; s < KD; ++s) qf[s] = qrow ? load32(qrow + 64 * s + 32 * half) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
+  }
+  const float c = a.alpha * a.s_q[bh] * a.s_k[bh] * kLog2e;
+  const float sv = a.s_v[bh];
+
+  // constant operand of the row-sum MFMA (see the header comment)
+  v8i ones;
+  {
+    const int r16 = lane % 16, g = lane / 16;
+    const bool on = ((r16 == 0 || r16 == 8) && (g == 0 || g == 2)) || ((r16 == 4 || r16 == 12) && (g == 1 || g == 3));
+    const int w = on ? 0x38383838 : 0;
+    ones = v8i{w, w, w, w, w, w, w, w};
+  }
+
+  v16f acc_o[D / 32];
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) acc_o[i] = v16f{};
+  v4f lacc = v4f{0.f, 0.f, 0.f, 0.f};
+  float m_run = -__builtin_inff();
+
+  const int ntiles = (N + 63) / 64;
+  const uint8_t* kbase = a.k8 + (size_t)bh * N * D;
+  const uint8_t* vbase = a.v8t + (size_t)bh * ntiles * D * 64;
+
+  for (int kt = 0; kt < ntiles; ++kt) {
+    // ---- stage K (64 x D, row-major) and V^T (D x 64) tiles into LDS ----
+    __syncthreads();
+#pragma unroll
+    for (int i = threadIdx.x; i < 64 * D / 16; i += 256) {
+      const int r = i / (D / 16), cc = i % (D / 16);
+      const int key = kt * 64 + r;
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (key < N) w = *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16);
+      *reinterpret_cast<u32x4*>(k_lds + r * KS + cc * 16) = w;
+    }
+#pragma unroll
+    for (int i = threadIdx.x; i < D * 4; i += 256) {
+      const int r = i / 4, cc = i % 4;
+      u32x4 w = *reinterpret_cast<const u32x4*>(vbase + (size_t)kt * D * 64 + r * 64 + cc * 16);
+      *reinterpret_cast<u32x4*>(v_lds + r * VS + cc * 16) = w;
+    }
+    __syncthreads();
+
+    // ---- S^T = K_8 Q_8^T for the two 32-key halves ----
+    v16f s0 = v16f{}, s1 = v16f{};
+#pragma unroll
+    for (int s = 0; s < KD; ++s) {
+      s0 = mfma_f8_32x32x64(load32(k_lds + ql * KS + 64 * s + 32 * half), qf[s], s0);
+      s1 = mfma_f8_32x32x64(load32(k_lds + (32 + ql) * KS + 64 * s + 32 * half), qf[s], s1);
+    }
+    // keys beyond N (last tile only) take no part
+    if (kt * 64 + 64 > N) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt * 64 + (r / 4) * 8 + half * 4 + (r % 4);
+        if (key >= N) s0[r] = -__builtin_inff();
+        if (key + 32 >= N) s1[r] = -__builtin_inff();
+      }
+    }
+
+    // ---- online softmax in the exp2 domain ----
+    float mx = s0[0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s0[r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s1[r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx);
+    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 0 on the first tile
+    const float bias = 8.0f - c * m_new;                                   // lifts the running max to 2^8
+    m_run = m_new;
+
+    v8i pf;
+#pragma unroll
+    for (int w = 0; w < 8; ++w) {
+      const v16f& src = w < 4 ? s0 : s1;
+      const int r = 4 * (w % 4);
+      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 0], c, bias));
+      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 1], c, bias));
+      const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 2], c, bias));
+      const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 3], c, bias));
+      int lo = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, 0, false);
+      pf[w] = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, lo, true);
+    }
+
+    // ---- rescale the running state, then accumulate l and O^T ----
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) acc_o[i] *= rescale;
+    lacc *= rescale;
+    lacc = mfma_f8_16x16x128(ones, pf, lacc);
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i)
+      acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (32 * i + ql) * VS + 32 * half), pf, acc_o[i]);
+  }
+
+  // ---- epilogue: O * s_v / l ----
+  if (row >= N + M) return;
+  const float inv = sv / lacc[0];
+  const size_t orow = row < N ? (((size_t)b * N + row) * a.H + h) * D
+                              : (((size_t)b * M + (row - N)) * a.H + h) * D;
+#pragma unroll
+  for (int i = 0; i < D / 32; ++i) {
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      const int d = 32 * i + 8 * g + 4 * half;
+      const float o0 = acc_o[i][4 * g + 0] * inv, o1 = acc_o[i][4 * g + 1] * inv;
+      const float o2 = acc_o[i][4 * g + 2] * inv, o3 = acc_o[i][4 * g + 3] * inv;
+      if constexpr (OUT_BF16) {
+        __bf16* op = (row < N ? (__bf16*)a.o_train : (__bf16*)a.o_test) + orow + d;
+        typedef __bf16 v4bf __attribute__((ext_vector_type(4)));
+        *reinterpret_cast<v4bf*>(op) = v4bf{(__bf16)o0, (__bf16)o1, (__bf16)o2, (__bf16)o3};
+      } else {
+        float* op = (row < N ? (float*)a.o_train : (float*)a.o_test) + orow + d;
+        *reinterpret_cast<v4f*>(op) = v4f{o0, o1, o2, o3};
+      }
+    }
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, float alpha, const uint8_t* q8_train,
+                           const uint8_t* q8_test, const uint8_t* k8, const uint8_t* v8t, const float* s_q,
+                           const float* s_k, const float* s_v, void* o_train, void* o_test, hipStream_t s) {
+  Fp8Args a;
+  a.B = B; a.H = H; a.N = N; a.M = M;
+  a.tiles = (N + M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.alpha = alpha;
+  a.q8_train = q8_train; a.q8_test = q8_test; a.k8 = k8; a.v8t = v8t;
+  a.s_q = s_q; a.s_k = s_k; a.s_v = s_v; a.o_train = o_train; a.o_test = o_test;
+  dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
+  if (D == 64) {
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<64, false>), grid, block, 0, s, a);
+  } else {
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<128, false>), grid, block, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+}  // namespace tfm

@@ -1,0 +1,62 @@
+// Internal declarations shared by the libtfm translation units (gfx950 only).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace tfm {
+
+typedef int v4i __attribute__((ext_vector_type(4)));
+typedef int v8i __attribute__((ext_vector_type(8)));
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef float v16f __attribute__((ext_vector_type(16)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kBlockKv = 64;          // keys per tile of both attention kernels
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).
+struct Fp8Workspace {
+  size_t amax;      // 3*B*H uint32: |x| maxima of Q_train, K, V as float bits
+  size_t scales;    // 3*B*H float: s_q, s_k, s_v
+  size_t q8_train;  // (B,H,N,D) codes
+  size_t q8_test;   // (B,H,M,D) codes
+  size_t k8;        // (B,H,N,D) codes
+  size_t v8t;       // (B,H,ceil(N/64),D,64) codes, tile-transposed (see attn_fp8.hip)
+  size_t total;
+};
+Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M);
+size_t v8t_bytes(int B, int H, int D, int N);
+
+// ---- launchers (return hipError_t of the launches) ----
+// Zero `n` uint32 words.
+hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s);
+// Per-(b,h) absmax of Q_train, K, V into amax[3][B][H] (must be zeroed first).
+hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, const void* q_train,
+                       const void* k, const void* v, uint32_t* amax, hipStream_t s);
+// Scales from amax: s = fl32(amax/448), 1 where that is 0; writes scales[3][B][H]
+// and, when the pointers are non-NULL, copies to s_q/s_k/s_v.
+hipError_t launch_scales(int BH, const uint32_t* amax, float* scales, float* s_q, float* s_k,
+                         float* s_v, hipStream_t s);
+// Quantize one (B,rows,H,D) tensor with per-(b,h) scales into (B,H,rows,D) codes.
+hipError_t launch_quantize_rows(int in_bf16, int B, int H, int D, int rows, const void* x,
+                                const float* scale, uint8_t* codes, hipStream_t s);
+// Quantize V (B,N,H,D) into the tile-transposed layout the FP8 kernel reads.
+hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, const void* v,
+                                   const float* scale, uint8_t* v8t, hipStream_t s);
+// Re-lay (B,H,N,D) V codes into the tile-transposed layout.
+hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8,
+                                   uint8_t* v8t, hipStream_t s);
+// Fused FP8 attention over the N+M query rows of every (b,h).
+hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, float alpha,
+                           const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8,
+                           const uint8_t* v8t, const float* s_q, const float* s_k,
+                           const float* s_v, void* o_train, void* o_test, hipStream_t s);
+// bf16 baseline attention over the N+M query rows of every (b,h).
+hipError_t launch_attn_bf16(int out_bf16, int B, int H, int D, int N, int M, float alpha,
+                            const void* q_train, const void* q_test, const void* k,
+                            const void* v, void* o_train, void* o_test, hipStream_t s);
+
+}  // namespace tfm

@@ -1,0 +1,295 @@
+// Per-head absmax quantization of Q, K, V to OCP e4m3fn on gfx950.
+//
+// Eq. (2) of the paper (Sec. 3): s = max|X^(h)| / 448 per head,
+// X_8 = rn_fp8(clamp(X / s, -448, 448)), fp32 scale; test queries use the
+// train-query scale.  Three passes, all HBM-bound streams of the inputs:
+//   1. amax_kernel   -- per-(tensor, b, h) max|x| with 16-byte loads; the
+//                       maximum of non-negative floats is taken on their bit
+//                       patterns as uint32 (order-preserving, exact), first in
+//                       LDS, then one global atomic max per head per block;
+//   2. scales_kernel -- s = fl32(amax / 448) (IEEE division), 1 where 0;
+//   3. quantize_*    -- fl32(x / s) (IEEE division), clamp, and the hardware
+//                       fp32 -> e4m3fn conversion, which rounds to nearest
+//                       even; codes go to (B,H,rows,D), or, for V on the fused
+//                       path, to the tile-transposed layout of attn_fp8.hip.
+#include "common.h"
+
+namespace tfm {
+namespace {
+
+constexpr int kThreads = 256;
+
+template <typename T> struct Vec;
+template <> struct Vec<float> { static constexpr int n = 4; };
+template <> struct Vec<uint16_t> { static constexpr int n = 8; };
+
+// |x| of the VEC elements of a 16-byte vector, as order-preserving uint32 bits.
+__device__ inline uint32_t absmax_bits(u32x4 w, float*) {
+  uint32_t a = max(w.x & 0x7fffffffu, w.y & 0x7fffffffu);
+  uint32_t b = max(w.z & 0x7fffffffu, w.w & 0x7fffffffu);
+  return max(a, b);
+}
+__device__ inline uint32_t absmax_bits(u32x4 w, uint16_t*) {
+  uint32_t m = 0;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    uint32_t hi = w[i] & 0x7fff0000u;
+    uint32_t lo = (w[i] << 16) & 0x7fff0000u;
+    m = max(m, max(hi, lo));
+  }
+  return m;
+}
+
+// The VEC elements of a 16-byte vector as floats.
+__device__ inline void unpack(u32x4 w, float* x, float*) {
+  x[0] = __uint_as_float(w.x); x[1] = __uint_as_float(w.y);
+  x[2] = __uint_as_float(w.z); x[3] = __uint_as_float(w.w);
+}
+__device__ inline void unpack(u32x4 w, float* x, uint16_t*) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    x[2 * i] = __uint_as_float(w[i] << 16);
+    x[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+
+// e4m3fn code of clamp(fl32(x / s), -448, 448), round to nearest even.
+// The division is the IEEE-correct fp32 division (HIP's default for '/');
+// v_cvt_pk_fp8_f32 rounds to nearest even and keeps the sign of zero.
+__device__ inline uint32_t codes4(const float* x, float s) {
+  float y[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) y[i] = __builtin_amdgcn_fmed3f(x[i] / s, -448.0f, 448.0f);
+  int w = __builtin_amdgcn_cvt_pk_fp8_f32(y[0], y[1], 0, false);
+  w = __builtin_amdgcn_cvt_pk_fp8_f32(y[2], y[3], w, true);
+  return (uint32_t)w;
+}
+
+// Thread -> (row offset, vector position) map shared by the row kernels: a
+// row of H*D elements is `vpr` 16-byte vectors; with vpr <= 256 each thread
+// keeps one fixed position (so one fixed head) and strides over rows.
+struct RowMap {
+  int vpr, lanes_per_row, rows_per_iter;
+  __device__ RowMap(int H, int D, int vec) {
+    vpr = H * D / vec;
+    lanes_per_row = vpr < kThreads ? vpr : kThreads;
+    rows_per_iter = kThreads / lanes_per_row;
+  }
+};
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void amax_kernel(int B, int H, int D, int N, int rows_per_chunk,
+                                                        const T* __restrict__ q, const T* __restrict__ k,
+                                                        const T* __restrict__ v, uint32_t* __restrict__ amax) {
+  extern __shared__ uint32_t smax[];  // H entries
+  constexpr int VEC = Vec<T>::n;
+  const int tensor = blockIdx.y, b = blockIdx.z;
+  const T* x = tensor == 0 ? q : (tensor == 1 ? k : v);
+  for (int i = threadIdx.x; i < H; i += kThreads) smax[i] = 0;
+  __syncthreads();
+  const RowMap rm(H, D, VEC);
+  const int t = threadIdx.x;
+  const int r0 = blockIdx.x * rows_per_chunk;
+  const int r1 = min(N, r0 + rows_per_chunk);
+  if (t < rm.rows_per_iter * rm.lanes_per_row) {
+    const int rr = t / rm.lanes_per_row;
+    for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
+      uint32_t m = 0;
+      const T* base = x + ((size_t)b * N) * H * D + (size_t)p * VEC;
+      for (int row = r0 + rr; row < r1; row += rm.rows_per_iter) {
+        u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)row * H * D);
+        m = max(m, absmax_bits(w, (T*)nullptr));
+      }
+      atomicMax(&smax[p * VEC / D], m);
+    }
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < H; i += kThreads)
+    if (smax[i]) atomicMax(&amax[((size_t)tensor * B + b) * H + i], smax[i]);
+}
+
+__global__ void fill_zero_kernel(uint32_t* p, int n) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
+}
+
+__global__ void scales_kernel(int BH, const uint32_t* __restrict__ amax, float* __restrict__ scales,
+                              float* s_q, float* s_k, float* s_v) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= 3 * BH) return;
+  float s = __uint_as_float(amax[i]) / 448.0f;
+  if (s == 0.0f) s = 1.0f;
+  scales[i] = s;
+  float* dst = i < BH ? s_q : (i < 2 * BH ? s_k : s_v);
+  if (dst) dst[i % BH] = s;
+}
+
+template <typename T>
+__global__ __launch_bounds__(kThreads) void quantize_rows_kernel(int H, int D, int rows, int rows_per_chunk,
+                                                                 const T* __restrict__ x,
+                                                                 const float* __restrict__ scale,
+                                                                 uint8_t* __restrict__ codes) {
+  constexpr int VEC = Vec<T>::n;
+  const int b = blockIdx.y;
+  const RowMap rm(H, D, VEC);
+  const int t = threadIdx.x;
+  const int r0 = blockIdx.x * rows_per_chunk;
+  const int r1 = min(rows, r0 + rows_per_chunk);
+  if (t >= rm.rows_per_iter * rm.lanes_per_row) return;
+  const int rr = t / rm.lanes_per_row;
+  for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
+    const int h = p * VEC / D, d0 = (p * VEC) % D;
+    const float s = scale[b * H + h];
+    const T* src = x + ((size_t)b * rows) * H * D + (size_t)p * VEC;
+    uint8_t* dst = codes + (((size_t)b * H + h) * rows) * D + d0;
+    for (int row = r0 + rr; row < r1; row += rm.rows_per_iter) {
+      u32x4 w = *reinterpret_cast<const u32x4*>(src + (size_t)row * H * D);
+      float xv[VEC];
+      unpack(w, xv, (T*)nullptr);
+      if constexpr (VEC == 4) {
+        *reinterpret_cast<uint32_t*>(dst + (size_t)row * D) = codes4(xv, s);
+      } else {
+        uint2 o;
+        o.x = codes4(xv, s);
+        o.y = codes4(xv + 4, s);
+        *reinterpret_cast<uint2*>(dst + (size_t)row * D) = o;
+      }
+    }
+  }
+}
+
+// Position of key kk (0..63) of a 64-key tile inside the tile-transposed V
+// layout: the PV product of attn_fp8.hip feeds lane half `hf` and byte j of
+// its B operand with key ((j%16)/4)*8 + hf*4 + j%4 + 32*(j/16) (the row
+// order of the QK^T accumulator), so V is stored in that order.
+__device__ inline int v_tile_pos(int kk) {
+  const int tile = kk >> 5, kp = kk & 31;
+  const int g = kp >> 3, hf = (kp >> 2) & 1, i = kp & 3;
+  return hf * 32 + tile * 16 + g * 4 + i;
+}
+
+// One block per (b*H + h, 64-key tile): codes of the tile's V rows (from
+// inputs or from (B,H,N,D) codes) transposed through LDS into
+// v8t[((b*H + h)*ntiles + tile)*D*64 + d*64 + pos].  Keys >= N get code 0.
+template <typename T, bool FROM_CODES>
+__global__ __launch_bounds__(kThreads) void v_tiles_kernel(int H, int D, int N, const T* __restrict__ src,
+                                                           const float* __restrict__ scale,
+                                                           uint8_t* __restrict__ v8t) {
+  __shared__ uint8_t tile_codes[128 * 64];
+  const int bh = blockIdx.y, kt = blockIdx.x;
+  const int b = bh / H, h = bh % H;
+  const int ntiles = (N + 63) / 64;
+  if constexpr (FROM_CODES) {
+    // src: (B,H,N,D) codes; 16 codes per thread-iteration
+    const int per_row = D / 16;
+    for (int i = threadIdx.x; i < 64 * per_row; i += kThreads) {
+      const int kk = i / per_row, c = i % per_row;
+      const int key = kt * 64 + kk;
+      u32x4 w = {0u, 0u, 0u, 0u};
+      if (key < N) w = *reinterpret_cast<const u32x4*>(src + ((size_t)bh * N + key) * D + c * 16);
+      const int pos = v_tile_pos(kk);
+#pragma unroll
+      for (int j = 0; j < 16; ++j) tile_codes[(c * 16 + j) * 64 + pos] = (uint8_t)(w[j / 4] >> (8 * (j % 4)));
+    }
+  } else {
+    constexpr int VEC = Vec<T>::n;
+    const float s = scale[bh];
+    const int per_row = D / VEC;
+    for (int i = threadIdx.x; i < 64 * per_row; i += kThreads) {
+      const int kk = i / per_row, c = i % per_row;
+      const int key = kt * 64 + kk;
+      uint32_t cw[VEC / 4];
+#pragma unroll
+      for (int j = 0; j < VEC / 4; ++j) cw[j] = 0u;
+      if (key < N) {
+        u32x4 w = *reinterpret_cast<const u32x4*>(src + (((size_t)b * N + key) * H + h) * D + c * VEC);
+        float xv[VEC];
+        unpack(w, xv, (T*)nullptr);
+#pragma unroll
+        for (int j = 0; j < VEC / 4; ++j) cw[j] = codes4(xv + 4 * j, s);
+      }
+      const int pos = v_tile_pos(kk);
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) tile_codes[(c * VEC + j) * 64 + pos] = (uint8_t)(cw[j / 4] >> (8 * (j % 4)));
+    }
+  }
+  __syncthreads();
+  uint8_t* dst = v8t + ((size_t)bh * ntiles + kt) * D * 64;
+  for (int i = threadIdx.x; i < D * 4; i += kThreads)
+    reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(tile_codes)[i];
+}
+
+int chunk_rows(int rows, int H, int D, int esize) {
+  // about 64 KiB of input per block
+  long per_row = (long)H * D * esize;
+  long r = (65536 + per_row - 1) / per_row;
+  if (r < 1) r = 1;
+  if (r > rows) r = rows > 0 ? rows : 1;
+  return (int)r;
+}
+
+}  // namespace
+
+hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(fill_zero_kernel, dim3((n + 255) / 256), dim3(256), 0, s, p, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, const void* q_train, const void* k,
+                       const void* v, uint32_t* amax, hipStream_t s) {
+  const int esize = in_bf16 ? 2 : 4;
+  const int rpc = chunk_rows(N, H, D, esize);
+  dim3 grid((N + rpc - 1) / rpc, 3, B);
+  size_t lds = (size_t)H * sizeof(uint32_t);
+  if (in_bf16)
+    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, B, H, D, N, rpc,
+                       (const uint16_t*)q_train, (const uint16_t*)k, (const uint16_t*)v, amax);
+  else
+    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, B, H, D, N, rpc,
+                       (const float*)q_train, (const float*)k, (const float*)v, amax);
+  return hipGetLastError();
+}
+
+hipError_t launch_scales(int BH, const uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
+                         hipStream_t s) {
+  hipLaunchKernelGGL(scales_kernel, dim3((3 * BH + 255) / 256), dim3(256), 0, s, BH, amax, scales, s_q, s_k,
+                     s_v);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_rows(int in_bf16, int B, int H, int D, int rows, const void* x, const float* scale,
+                                uint8_t* codes, hipStream_t s) {
+  if (rows <= 0) return hipSuccess;
+  const int esize = in_bf16 ? 2 : 4;
+  const int rpc = chunk_rows(rows, H, D, esize);
+  dim3 grid((rows + rpc - 1) / rpc, B);
+  if (in_bf16)
+    hipLaunchKernelGGL(quantize_rows_kernel<uint16_t>, grid, dim3(kThreads), 0, s, H, D, rows, rpc,
+                       (const uint16_t*)x, scale, codes);
+  else
+    hipLaunchKernelGGL(quantize_rows_kernel<float>, grid, dim3(kThreads), 0, s, H, D, rows, rpc,
+                       (const float*)x, scale, codes);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, const void* v, const float* scale,
+                                   uint8_t* v8t, hipStream_t s) {
+  dim3 grid((N + 63) / 64, B * H);
+  if (in_bf16)
+    hipLaunchKernelGGL((v_tiles_kernel<uint16_t, false>), grid, dim3(kThreads), 0, s, H, D, N,
+                       (const uint16_t*)v, scale, v8t);
+  else
+    hipLaunchKernelGGL((v_tiles_kernel<float, false>), grid, dim3(kThreads), 0, s, H, D, N, (const float*)v,
+                       scale, v8t);
+  return hipGetLastError();
+}
+
+hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8, uint8_t* v8t, hipStream_t s) {
+  dim3 grid((N + 63) / 64, B * H);
+  hipLaunchKernelGGL((v_tiles_kernel<uint8_t, true>), grid, dim3(kThreads), 0, s, H, D, N, v8,
+                     (const float*)nullptr, v8t);
+  return hipGetLastError();
+}
+
+}  // namespace tfm

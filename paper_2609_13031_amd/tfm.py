@@ -1,0 +1,240 @@
+"""Python binding of libtfm (include/tfm.h): argument marshalling only.
+
+Every function has the name of the C entry point it calls, takes and returns
+torch tensors on the current HIP device, enqueues on torch's current stream
+and raises ``TfmError`` with the library's status text when the library
+rejects a call.  Nothing here computes any part of the method: all of it runs
+in the HIP kernels of libtfm.so, which must have been built (see
+``__graft_entry__.build``); ``lib()`` raises if it is missing.
+"""
+import ctypes
+import math
+import os
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtfm.so")
+
+TFM_F32 = 0
+TFM_BF16 = 1
+_DTYPES = {torch.float32: TFM_F32, torch.bfloat16: TFM_BF16}
+
+# name -> (restype, argtypes), in the order of include/tfm.h
+_c_int, _c_size, _c_float, _p = ctypes.c_int, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
+SIGNATURES = {
+    "tfm_status_string": (ctypes.c_char_p, [_c_int]),
+    "tfm_version": (_c_int, []),
+    "tfm_quantize_workspace_bytes": (_c_size, [_c_int, _c_int]),
+    "tfm_quantize_qkv_per_head": (_c_int, [_c_int] * 6 + [_p] * 12 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_workspace_bytes": (_c_size, [_c_int] * 5),
+    "tfm_icl_attention_fp8": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 7 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_quantize": (_c_int, [_c_int] * 6 + [_p] * 5 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_attend": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 3 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_prequantized_workspace_bytes": (_c_size, [_c_int] * 4),
+    "tfm_icl_attention_fp8_prequantized": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 10 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_block_kv": (_c_int, [_c_int]),
+    "tfm_icl_attention_bf16": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 6 + [_p]),
+}
+
+
+class TfmError(RuntimeError):
+    def __init__(self, status, where):
+        self.status = status
+        super().__init__("%s: %s" % (where, lib().tfm_status_string(status).decode()))
+
+
+_lib = None
+
+
+def lib():
+    """The loaded libtfm (ctypes.CDLL); raises if the library has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libtfm.so not found at %s: build it with __graft_entry__.build()" % LIB_PATH)
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            f = getattr(L, name)
+            f.restype, f.argtypes = res, args
+        _lib = L
+    return _lib
+
+
+def _ptr(t):
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _call(name, *args):
+    st = getattr(lib(), name)(*args)
+    if st != 0:
+        raise TfmError(st, name)
+
+
+def _shape_bnhd(x, what):
+    if x.dim() != 4:
+        raise ValueError("%s must be (B, rows, H, D)" % what)
+    return x.shape
+
+
+def _check_inputs(tensors, dtype=None):
+    dev = None
+    for name, t in tensors.items():
+        if t is None:
+            continue
+        if not t.is_cuda:
+            raise ValueError("%s must be a GPU tensor" % name)
+        if not t.is_contiguous():
+            raise ValueError("%s must be contiguous" % name)
+        if dtype is not None and t.dtype != dtype:
+            raise ValueError("%s must be %s" % (name, dtype))
+        if dev is None:
+            dev = t.device
+        elif t.device != dev:
+            raise ValueError("all tensors must be on one device")
+    return dev
+
+
+def _qkv_dims(q_train, k, v, q_test):
+    B, N, H, D = _shape_bnhd(q_train, "q_train")
+    if tuple(k.shape) != (B, N, H, D) or tuple(v.shape) != (B, N, H, D):
+        raise ValueError("k and v must have the shape of q_train")
+    M = 0
+    if q_test is not None:
+        Bt, M, Ht, Dt = _shape_bnhd(q_test, "q_test")
+        if (Bt, Ht, Dt) != (B, H, D):
+            raise ValueError("q_test must be (B, M, H, D)")
+        if M == 0:
+            q_test = None
+    return B, H, D, N, M, q_test
+
+
+def _alpha(alpha, D):
+    return float(1.0 / math.sqrt(D)) if alpha is None else float(alpha)
+
+
+def tfm_version():
+    return lib().tfm_version()
+
+
+def tfm_icl_attention_fp8_block_kv(D):
+    return lib().tfm_icl_attention_fp8_block_kv(int(D))
+
+
+def tfm_quantize_workspace_bytes(B, H):
+    return lib().tfm_quantize_workspace_bytes(B, H)
+
+
+def tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M):
+    return lib().tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
+
+
+def tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N):
+    return lib().tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
+
+
+def tfm_quantize_qkv_per_head(q_train, k, v, q_test=None):
+    """Eq. (2) per (b, h): returns dict q8_train, k8, v8, q8_test ((B,H,rows,D) uint8) and s_q, s_k, s_v ((B,H) fp32)."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if q_train.dtype not in _DTYPES:
+        raise ValueError("inputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
+    u8 = dict(dtype=torch.uint8, device=dev)
+    out = {"q8_train": torch.empty((B, H, N, D), **u8), "k8": torch.empty((B, H, N, D), **u8),
+           "v8": torch.empty((B, H, N, D), **u8),
+           "q8_test": torch.empty((B, H, M, D), **u8) if M else None,
+           "s_q": torch.empty((B, H), dtype=torch.float32, device=dev),
+           "s_k": torch.empty((B, H), dtype=torch.float32, device=dev),
+           "s_v": torch.empty((B, H), dtype=torch.float32, device=dev)}
+    nws = tfm_quantize_workspace_bytes(B, H)
+    ws = torch.empty(nws, **u8)
+    _call("tfm_quantize_qkv_per_head", _DTYPES[q_train.dtype], B, H, D, N, M, _ptr(q_train), _ptr(k), _ptr(v),
+          _ptr(q_test), _ptr(out["q8_train"]), _ptr(out["k8"]), _ptr(out["v8"]), _ptr(out["q8_test"]),
+          _ptr(out["s_q"]), _ptr(out["s_k"]), _ptr(out["s_v"]), _ptr(ws), nws, _stream())
+    if out["q8_test"] is None:
+        out["q8_test"] = torch.empty((B, H, 0, D), **u8)
+    return out
+
+
+def _outputs(B, H, D, N, M, out_dtype, dev, out):
+    if out is not None:
+        o_tr, o_te = out
+    else:
+        o_tr = torch.empty((B, N, H, D), dtype=out_dtype, device=dev)
+        o_te = torch.empty((B, M, H, D), dtype=out_dtype, device=dev)
+    return o_tr, o_te
+
+
+def tfm_icl_attention_fp8(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None, workspace=None):
+    """Quantize (Eq. (2)) and run both ICL calls in FP8; returns (o_train (B,N,H,D), o_test (B,M,H,D))."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    nws = tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
+    ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
+    _call("tfm_icl_attention_fp8", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+          _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _ptr(ws),
+          ws.numel(), _stream())
+    return o_tr, o_te
+
+
+def tfm_icl_attention_fp8_quantize(q_train, k, v, q_test=None, workspace=None):
+    """First stage of tfm_icl_attention_fp8: quantize into a workspace (returned)."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if q_train.dtype not in _DTYPES:
+        raise ValueError("inputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
+    nws = tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
+    ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
+    _call("tfm_icl_attention_fp8_quantize", _DTYPES[q_train.dtype], B, H, D, N, M, _ptr(q_train), _ptr(k), _ptr(v),
+          _ptr(q_test), _ptr(ws), ws.numel(), _stream())
+    return ws
+
+
+def tfm_icl_attention_fp8_attend(workspace, B, H, D, N, M, alpha=None, out_dtype=torch.float32, out=None):
+    """Second stage of tfm_icl_attention_fp8: both ICL calls from a quantized workspace."""
+    if out_dtype not in _DTYPES:
+        raise ValueError("outputs must be float32 or bfloat16")
+    dev = _check_inputs({"workspace": workspace}, torch.uint8)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    _call("tfm_icl_attention_fp8_attend", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D), _ptr(o_tr),
+          _ptr(o_te if M else None), _ptr(workspace), workspace.numel(), _stream())
+    return o_tr, o_te
+
+
+def tfm_icl_attention_fp8_prequantized(q8_train, k8, v8, q8_test, s_q, s_k, s_v, alpha=None,
+                                       out_dtype=torch.float32, out=None, workspace=None):
+    """Both ICL calls on codes/scales from tfm_quantize_qkv_per_head; returns (o_train, o_test)."""
+    B, H, N, D = q8_train.shape
+    M = 0 if q8_test is None else q8_test.shape[2]
+    if M == 0:
+        q8_test = None
+    dev = _check_inputs({"q8_train": q8_train, "k8": k8, "v8": v8, "q8_test": q8_test}, torch.uint8)
+    _check_inputs({"s_q": s_q, "s_k": s_k, "s_v": s_v}, torch.float32)
+    for name, t in (("k8", k8), ("v8", v8)):
+        if tuple(t.shape) != (B, H, N, D):
+            raise ValueError("%s must be (B, H, N, D)" % name)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    nws = tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
+    ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
+    _call("tfm_icl_attention_fp8_prequantized", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+          _ptr(q8_train), _ptr(k8), _ptr(v8), _ptr(q8_test), _ptr(s_q), _ptr(s_k), _ptr(s_v), _ptr(o_tr),
+          _ptr(o_te if M else None), _ptr(ws), ws.numel(), _stream())
+    return o_tr, o_te
+
+
+def tfm_icl_attention_bf16(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None):
+    """The bf16 baseline of both ICL calls; returns (o_train, o_test)."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if out_dtype not in _DTYPES:
+        raise ValueError("outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, torch.bfloat16)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    _call("tfm_icl_attention_bf16", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D), _ptr(q_train), _ptr(k),
+          _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
+    return o_tr, o_te

@@ -1,0 +1,131 @@
+"""Shared helpers of the GPU parity tests: device transfer, row sampling and
+the stated tolerances (T1 against the oracle's kernel model O_qp, T2 against
+Eq. (1) on the dequantized inputs O_q)."""
+import numpy as np
+import torch
+
+from oracle import attention as OA
+from oracle.e4m3 import decode
+
+# T1 -- FP8 path vs O_qp (the one-pass kernel replayed in fp64), elementwise:
+#   |dO| <= 1.01 * tie allowance + 1e-5 * RMS(O_qp) + 1e-6 * |O_qp|.
+# It applies where every FP8 MFMA dot product is exact (inputs whose codes
+# span a narrow range, see ``narrow_range_inputs``): the kernel then differs
+# from O_qp by fp32 arithmetic only.  Its exponent c*S + 8 - c*m is off by at
+# most ~1e-6 (fp32 c: 3 roundings of |c S| <= 1; fp32 bias and fma: 2^-21
+# each near 8), and v_exp_f32 adds < 1 ulp, so P~ moves by < 1e-6 relative:
+# a key can round to the other e4m3 neighbour only if O_qp's P~ lies within
+# TIE_REL (4x margin) of a rounding midpoint; the oracle's tie allowance
+# bounds the effect of all such keys.  Everything else is fp32 noise.
+TIE_REL = 2.0 ** -18
+T1_MAX, T1_RELF, T1_OUTLIER, T1_OUTLIER_FRAC = 1e-2, 1e-4, 2e-3, 1e-3   # reported only
+
+# The FP8 MFMA of gfx950 (v_mfma_f32_*_f8f6f4) does not round its dot product
+# exactly: products are aligned to the largest one and truncated, so a 64-term
+# dot product can be off by up to ~2.3e-4 of sum |a_k b_k| (measured with
+# random full-range e4m3 operands; a narrow exponent range is exact), and each
+# accumulation into C loses about one fp32 ulp (truncation).  EPS_DOT bounds
+# the first with a 2x margin, EPS_ACC the second per key tile.
+EPS_DOT = 2.0 ** -11
+EPS_ACC = 2.0 ** -22
+# T1' -- on general inputs the FP8 path stays within relF 1e-2 of O_qp (the
+# accumulator noise above gives ~1e-3; a dropped key tile or a missing rescale
+# gives 0.17 and more), and elementwise within T2' of O_q.
+T1P_RELF = 1e-2
+
+
+def t1_metrics(got, ref):
+    d = np.abs(np.asarray(got, np.float64) - ref)
+    rms = np.sqrt(np.mean(ref ** 2))
+    return {"max_over_rms": d.max() / rms,
+            "relF": np.linalg.norm(d) / np.linalg.norm(ref),
+            "outlier_frac": np.mean(d > T1_OUTLIER * rms)}
+
+
+def assert_t1(got, ref, allowance, what=""):
+    got = np.asarray(got, np.float64)
+    rms = np.sqrt(np.mean(ref ** 2))
+    err = np.abs(got - ref)
+    tol = 1.01 * allowance + 1e-5 * rms + 1e-6 * np.abs(ref)
+    assert np.all(err <= tol), (what, (err / tol).max(), t1_metrics(got, ref))
+    return t1_metrics(got, ref)
+
+
+def p_rounding_bound(q8, k8, v_hat, c, eps_dot=0.0, n_tiles=0):
+    """Elementwise bound on |O - O_q| for the one-pass FP8 kernel (rows of q8).
+
+    With p_j = 2^(c (s_j - max s) + 8) the exact lifted weights, a weight the
+    kernel uses is w_j = g * p_j * 2^(c d_j) (1 + r_j) + z_j: g a factor common
+    to the row (it cancels), |d_j| <= eps_dot * sum_k |q_k k_jk| the error of
+    the QK^T dot product, |r_j| <= 2^-4 (half an e4m3 ulp, normal range) and
+    |z_j| <= 2^-10 (half the subnormal step; rescaling by 2^(c(m_old-m)) <= 1
+    only shrinks it).  Then O - O_q = sum_j (w_j/g - p_j)(v_j - O_q) / sum_j w_j/g.
+    The PV and row-sum dot products add eps_dot of sum_j p_j |v_j| / sum p
+    each, and n_tiles accumulations into C add EPS_ACC per tile of the same.
+    With eps_dot = 0 and n_tiles = 0 this is the bound of O_qp itself.
+    """
+    s = q8 @ k8.T
+    p = np.exp2(c * (s - s.max(axis=1, keepdims=True)) + 8.0)
+    psum = p.sum(axis=1)
+    o = (p @ v_hat) / psum[:, None]
+    a = np.abs(q8) @ np.abs(k8).T
+    e = p * ((1 + 2.0 ** -4) * np.exp2(c * eps_dot * a) - 1) + 2.0 ** -10 * np.exp2(c * eps_dot * a.max(axis=1))[:, None]
+    num = np.empty_like(o)
+    for ch in range(v_hat.shape[1]):
+        num[:, ch] = np.einsum("rj,rj->r", e, np.abs(v_hat[None, :, ch] - o[:, ch][:, None]))
+    den = psum - e.sum(axis=1)
+    bound = np.where(den[:, None] > 0, num / np.where(den > 0, den, 1.0)[:, None], np.inf)
+    pv = (p @ np.abs(v_hat)) / psum[:, None]
+    bound += (2 * eps_dot + n_tiles * EPS_ACC) * (pv + np.abs(o))
+    return o, bound
+
+
+def assert_t2(got, qz, alpha, b, h, q8_rows, slack=1.25, eps_dot=EPS_DOT):
+    """T2': |O_gpu - O_q| <= 1.25 * p_rounding_bound(eps_dot) + 1e-5 * RMS, elementwise."""
+    c = float(alpha) * float(qz["s_q"][b, h]) * float(qz["s_k"][b, h]) * OA.LOG2E
+    k8 = decode(qz["k8"][b, h])
+    v_hat = decode(qz["v8"][b, h]) * float(qz["s_v"][b, h])
+    n_tiles = (k8.shape[0] + 63) // 64
+    o, bnd = p_rounding_bound(decode(q8_rows), k8, v_hat, c, eps_dot, n_tiles)
+    rms = np.sqrt(np.mean(o ** 2))
+    err = np.abs(np.asarray(got, np.float64) - o)
+    assert np.all(err <= slack * bnd + 1e-5 * rms), (err / (bnd + 1e-30)).max()
+    return err.max() / rms
+
+
+def assert_t1p(got, ref, what=""):
+    """T1': statistical agreement with O_qp on general inputs (relF only)."""
+    m = t1_metrics(got, ref)
+    assert m["relF"] <= T1P_RELF, (what, m)
+    return m
+
+
+def narrow_range_inputs(B, N, M, H, D, seed):
+    """Inputs whose e4m3 codes all have magnitudes in [224, 448] (|x| in [amax/2, amax]
+    with random signs), so every FP8 MFMA dot product of the kernel is exact:
+    Q and K products span two binades, and with alpha = 1/sqrt(D) the lifted
+    P_8 lie in [2^6, 2^8], so the P V products span a few binades too."""
+    rng = np.random.default_rng(seed)
+    def draw(rows):
+        mag = rng.uniform(0.5, 1.0, (B, rows, H, D)).astype(np.float32)
+        return (mag * rng.choice(np.array([-1.0, 1.0], np.float32), size=mag.shape)).astype(np.float32)
+    q = draw(N + M)
+    return {"q_train": q[:, :N].copy(), "k": draw(N), "v": draw(N), "q_test": q[:, N:].copy()}
+
+
+def sample_rows(n, k, seed, block=128):
+    """First/last rows, rows on both sides of query-tile boundaries and random rows (sorted, unique)."""
+    rng = np.random.default_rng(seed)
+    pick = {0, n - 1}
+    for t in range(block, n, block * max(1, (n // block) // 8)):
+        pick.update((t - 1, t))
+    pick.update(rng.integers(0, n, size=max(0, k - len(pick))).tolist())
+    return np.array(sorted(x for x in pick if 0 <= x < n), dtype=np.int64)
+
+
+def to_dev(x, dtype):
+    return torch.from_numpy(np.ascontiguousarray(x)).to(dtype).cuda()
+
+
+def gpu_inputs(x, dtype):
+    return {k: to_dev(v, dtype) for k, v in x.items()}

@@ -1,0 +1,104 @@
+"""C-ABI checks that need no GPU: the library loads, exports every entry point
+of include/tfm.h, and rejects bad arguments before enqueuing anything."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_13031_amd import tfm
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(os.path.abspath(__file__))), "include", "tfm.h")
+
+
+def header_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(tfm_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    L = tfm.lib()
+    names = header_functions()
+    assert len(names) == 12
+    for n in names:
+        assert hasattr(L, n), n
+    assert set(names) == set(tfm.SIGNATURES)
+
+
+def test_status_strings_and_version():
+    L = tfm.lib()
+    assert L.tfm_status_string(0) == b"TFM_OK"
+    for st in range(1, 9):
+        assert L.tfm_status_string(st).startswith(b"TFM_ERR_")
+    assert L.tfm_status_string(99) == b"TFM_ERR_UNKNOWN"
+    assert tfm.tfm_version() == 100
+
+
+def test_block_kv_and_workspace_queries():
+    assert tfm.tfm_icl_attention_fp8_block_kv(64) == 64
+    assert tfm.tfm_icl_attention_fp8_block_kv(128) == 64
+    assert tfm.tfm_icl_attention_fp8_block_kv(96) == 0
+    assert tfm.tfm_quantize_workspace_bytes(2, 6) == 512
+    assert tfm.tfm_quantize_workspace_bytes(0, 6) == 0
+    # codes of Q_train, Q_test, K (N or M x D per head), V tiles (ceil(N/64)*64*D), amax, scales
+    B, H, D, N, M = 2, 6, 64, 65536, 16384
+    want = 256 + 256 + B * H * (N * D + M * D + N * D + N * D)
+    assert tfm.tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M) == want
+    assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 64, 65, 0) >= 256 * 2 + 65 * 64 * 2 + 128 * 64
+    assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 96, 10, 0) == 0
+    assert tfm.tfm_icl_attention_fp8_prequantized_workspace_bytes(1, 2, 128, 100) == 2 * 128 * 128
+
+
+FAKE = 0x10000          # aligned, never dereferenced: validation fails first
+MIS = 0x10008           # 8-byte aligned only
+
+
+def fp8_call(**kw):
+    a = dict(in_dtype=1, out_dtype=0, B=1, H=2, D=64, N=100, M=10, alpha=0.125, q_train=FAKE, k=FAKE, v=FAKE,
+             q_test=FAKE, o_train=FAKE, o_test=FAKE, ws=FAKE, nws=1 << 40)
+    a.update(kw)
+    return tfm.lib().tfm_icl_attention_fp8(a["in_dtype"], a["out_dtype"], a["B"], a["H"], a["D"], a["N"], a["M"],
+                                           a["alpha"], a["q_train"], a["k"], a["v"], a["q_test"], a["o_train"],
+                                           a["o_test"], a["ws"], a["nws"], None)
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(B=0), 2), (dict(H=0), 2), (dict(N=0), 2), (dict(M=-1), 2), (dict(B=70000), 2),
+    (dict(N=2 ** 31 - 100, M=1000), 2), (dict(D=96), 4), (dict(D=32), 4),
+    (dict(in_dtype=2), 3), (dict(out_dtype=7), 3),
+    (dict(alpha=0.0), 8), (dict(alpha=-1.0), 8), (dict(alpha=float("nan")), 8), (dict(alpha=float("inf")), 8),
+    (dict(q_train=None), 1), (dict(k=None), 1), (dict(ws=None), 1), (dict(q_test=None), 1), (dict(o_test=None), 1),
+    (dict(v=MIS), 5), (dict(o_train=MIS), 5), (dict(q_test=MIS), 5),
+    (dict(nws=1000), 6),
+])
+def test_fp8_validation_errors(kw, status):
+    assert fp8_call(**kw) == status
+
+
+def test_validation_order_and_m_zero_allows_null_test_pointers():
+    # M == 0: NULL test pointers are fine, so the next failing check (workspace) reports
+    assert fp8_call(M=0, q_test=None, o_test=None, nws=10) == 6
+    # shape errors take precedence over pointer errors
+    assert fp8_call(B=0, q_train=None) == 2
+
+
+def test_quantize_and_bf16_and_prequantized_validation():
+    L = tfm.lib()
+    q = lambda **kw: L.tfm_quantize_qkv_per_head(kw.get("dt", 0), kw.get("B", 1), 2, kw.get("D", 64), 50, 0,
+                                                 FAKE, FAKE, FAKE, None, FAKE, FAKE, kw.get("v8", FAKE), None,
+                                                 FAKE, FAKE, FAKE, FAKE, kw.get("nws", 1 << 20), None)
+    assert q(dt=5) == 3 and q(B=0) == 2 and q(D=100) == 4 and q(v8=None) == 1 and q(v8=MIS) == 5 and q(nws=8) == 6
+    b = lambda **kw: L.tfm_icl_attention_bf16(kw.get("out", 1), 1, 2, 64, kw.get("N", 50), 3, kw.get("alpha", 0.1),
+                                              FAKE, FAKE, FAKE, kw.get("qt", FAKE), FAKE, FAKE, None)
+    assert b(out=3) == 3 and b(N=0) == 2 and b(alpha=-2.0) == 8 and b(qt=None) == 1 and b(qt=MIS) == 5
+    qs = lambda **kw: L.tfm_icl_attention_fp8_quantize(1, 1, 2, 64, 50, kw.get("M", 3), FAKE, FAKE, FAKE,
+                                                       kw.get("qt", FAKE), FAKE, kw.get("nws", 1 << 30), None)
+    assert qs(qt=None) == 1 and qs(M=0, qt=None, nws=10) == 6 and qs(qt=MIS) == 5
+    at = lambda **kw: L.tfm_icl_attention_fp8_attend(0, 1, 2, 64, 50, 3, kw.get("alpha", 0.1), FAKE,
+                                                     kw.get("ot", FAKE), FAKE, kw.get("nws", 1 << 30), None)
+    assert at(alpha=0.0) == 8 and at(ot=None) == 1 and at(nws=1) == 6
+    p = lambda **kw: L.tfm_icl_attention_fp8_prequantized(0, 1, 2, 64, 50, 0, 0.1, FAKE, FAKE, FAKE, None, FAKE,
+                                                          kw.get("sk", FAKE), FAKE, FAKE, None, FAKE,
+                                                          kw.get("nws", 1 << 20), None)
+    assert p(sk=None) == 1 and p(nws=100) == 6

@@ -1,0 +1,255 @@
+"""GPU parity of the FP8 and bf16 ICL attention entry points with the oracle.
+
+FP8: against O_qp (the oracle's one-pass kernel model) within T1 and against
+O_q (Eq. (1) on the dequantized inputs) within the e4m3 P-rounding bound T2,
+on every workload (full-size ones on sampled rows: each output row depends
+only on its query and all keys, so a sampled row is checked exactly), plus
+edge shapes, closed forms and invariances.  bf16: against Eq. (1) in fp64."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import quantize as OQ
+from oracle.e4m3 import decode
+from paper_2609_13031_amd import tfm
+from paper_2609_13031_amd.workloads import WORKLOADS, Workload, generate
+from parity import (EPS_ACC, EPS_DOT, TIE_REL, assert_t1, assert_t1p, assert_t2, gpu_inputs, narrow_range_inputs,
+                    sample_rows)
+
+pytestmark = pytest.mark.gpu
+BKV = 64
+
+
+def fp8(g, w, out_dtype=torch.float32):
+    o = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha, out_dtype=out_dtype)
+    torch.cuda.synchronize()
+    return o[0].float().cpu().numpy(), o[1].float().cpu().numpy()
+
+
+def check_workload(w, rows_tr=None, rows_te=None, t2_rows=None):
+    print("workload", w, flush=True)
+    x = generate(w)
+    g = gpu_inputs(x, torch.float32 if w.dtype == "f32" else torch.bfloat16)
+    o_tr, o_te = fp8(g, w)
+    del g
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    r_tr, r_te = OA.icl_attention_fp8_kernel_model(qz, w.alpha, BKV, rows_tr, rows_te)
+    rt = np.arange(w.N) if rows_tr is None else rows_tr
+    re = np.arange(w.M) if rows_te is None else rows_te
+    worst = 0.0
+    for b in range(w.B):
+        for h in range(w.H):
+            for o, r, rows, q8 in ((o_tr, r_tr, rt, qz["q8_train"]), (o_te, r_te, re, qz.get("q8_test"))):
+                if len(rows) == 0:
+                    continue
+                m = assert_t1p(o[b, rows, h], r[b, :, h], (b, h, len(rows)))
+                worst = max(worst, m["relF"])
+                sub = rows if t2_rows is None else rows[:t2_rows]
+                assert_t2(o[b, sub, h], qz, w.alpha, b, h, q8[b, h, sub])
+    print("worst relF vs O_qp: %.3e" % worst)
+
+
+@pytest.mark.parametrize("B,H,D,N,M", [(1, 2, 64, 512, 128), (2, 3, 64, 1000, 77), (1, 2, 128, 700, 64)])
+def test_exact_mfma_regime_matches_kernel_model_tightly(B, H, D, N, M):
+    # codes in [224, 448] and a small softmax scale keep every FP8 MFMA dot
+    # product exact, so the kernel must agree with O_qp to fp32 rounding (T1)
+    x = narrow_range_inputs(B, N, M, H, D, seed=N + D)
+    w = Workload("narrow", B=B, H=H, D=D, N=N, M=M, dtype="f32")
+    alpha = 0.025
+    g = gpu_inputs(x, torch.float32)
+    o = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=alpha)
+    o_tr, o_te = o[0].cpu().numpy(), o[1].cpu().numpy()
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    (r_tr, a_tr), (r_te, a_te) = OA.icl_attention_fp8_kernel_model(qz, np.float32(alpha), BKV, tie_rel=TIE_REL)
+    for b in range(B):
+        for h in range(H):
+            m1 = assert_t1(o_tr[b, :, h], r_tr[b, :, h], a_tr[b, :, h], ("train", b, h))
+            m2 = assert_t1(o_te[b, :, h], r_te[b, :, h], a_te[b, :, h], ("test", b, h))
+            assert_t2(o_tr[b, :, h], qz, np.float32(alpha), b, h, qz["q8_train"][b, h], eps_dot=0.0)
+    print("T1 metrics (last head):", m1, m2)
+
+
+def test_tiny_full():
+    check_workload(WORKLOADS["tiny"])
+
+
+def test_threshold_sampled():
+    w = WORKLOADS["threshold"]
+    check_workload(w, sample_rows(w.N, 256, 1), sample_rows(w.M, 128, 2), t2_rows=64)
+
+
+def test_many_tables_sampled():
+    w = WORKLOADS["many_tables"]
+    check_workload(w, sample_rows(w.N, 48, 3), sample_rows(w.M, 24, 4), t2_rows=16)
+
+
+def test_mid_full_size_sampled():
+    w = WORKLOADS["mid"]
+    check_workload(w, sample_rows(w.N, 64, 5), sample_rows(w.M, 32, 6), t2_rows=8)
+
+
+def test_large_full_size_sampled():
+    w = WORKLOADS["large"]
+    check_workload(w, sample_rows(w.N, 24, 7), sample_rows(w.M, 12, 8), t2_rows=4)
+
+
+@pytest.mark.parametrize("B,H,D,N,M,dtype", [
+    (1, 1, 64, 1, 1, "f32"), (1, 2, 64, 63, 0, "bf16"), (2, 1, 64, 64, 5, "f32"), (1, 3, 64, 65, 130, "bf16"),
+    (1, 1, 128, 1, 0, "bf16"), (1, 2, 128, 129, 17, "f32"), (3, 2, 128, 200, 255, "bf16"), (1, 1, 64, 1000, 1, "bf16"),
+])
+def test_edge_shapes(B, H, D, N, M, dtype):
+    check_workload(Workload("edge", B=B, H=H, D=D, N=N, M=M, dtype=dtype, seed=B * 1000 + N + M))
+
+
+def test_identical_keys_give_mean_of_v_and_constant_v_is_returned():
+    rng = np.random.default_rng(20)
+    B, N, H, D, M = 1, 300, 2, 64, 40
+    q = rng.standard_normal((B, N + M, H, D)).astype(np.float32) * 3
+    k = np.repeat(rng.standard_normal((B, 1, H, D)).astype(np.float32), N, axis=1)
+    v = rng.standard_normal((B, N, H, D)).astype(np.float32)
+    x = {"q_train": q[:, :N], "k": k, "v": v, "q_test": q[:, N:]}
+    w = Workload("closed", B=B, H=H, D=D, N=N, M=M, dtype="f32")
+    o_tr, o_te = fp8(gpu_inputs(x, torch.float32), w)
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    v_hat = OA.dequantize(qz["v8"], qz["s_v"])
+    mean_v = v_hat.mean(axis=1)                                          # (B, H, D)
+    # every lifted weight is exactly 2^8; only the FP8 MFMA accumulation of P V and of l errs
+    rel = 2 * EPS_DOT + ((N + 63) // 64) * EPS_ACC
+    for o in (o_tr, o_te):
+        assert np.all(np.abs(o - mean_v[:, None]) <= rel * (np.abs(v_hat).mean(axis=1)[:, None] + np.abs(mean_v[:, None])))
+    x["v"] = np.full_like(v, 1.75)
+    x["k"] = rng.standard_normal((B, N, H, D)).astype(np.float32) * 4
+    o_tr, o_te = fp8(gpu_inputs(x, torch.float32), w)
+    for o in (o_tr, o_te):
+        assert np.allclose(o, 1.75, rtol=2 * rel, atol=0)
+
+
+def test_one_hot_rows():
+    # key 11 matches every query far better than the rest: the output is its V row
+    B, N, H, D, M = 1, 256, 1, 64, 8
+    rng = np.random.default_rng(21)
+    k = rng.standard_normal((B, N, H, D)).astype(np.float32) * 0.01
+    k[0, 11, 0, :] = 1.0
+    q = np.ones((B, N + M, H, D), np.float32) * 4.0
+    v = rng.standard_normal((B, N, H, D)).astype(np.float32)
+    x = {"q_train": q[:, :N], "k": k, "v": v, "q_test": q[:, N:]}
+    o_tr, o_te = fp8(gpu_inputs(x, torch.float32), Workload("onehot", B=B, H=H, D=D, N=N, M=M, dtype="f32"))
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    v11 = OA.dequantize(qz["v8"], qz["s_v"])[0, 11, 0]
+    assert np.allclose(o_tr[0, :, 0], v11, rtol=1e-6, atol=1e-6)
+    assert np.allclose(o_te[0, :, 0], v11, rtol=1e-6, atol=1e-6)
+
+
+@pytest.fixture(scope="module")
+def thr():
+    w = WORKLOADS["threshold"].with_(N=4000, M=700)
+    x = generate(w)
+    return w, x, gpu_inputs(x, torch.bfloat16)
+
+
+def test_batch_invariance_of_test_rows(thr):
+    # the train-query scale makes a test row's output independent of the other test rows
+    w, x, g = thr
+    _, full = fp8(g, w)
+    perm = np.random.default_rng(22).permutation(w.M)[:123]
+    g2 = dict(g)
+    g2["q_test"] = g["q_test"][:, torch.from_numpy(perm).cuda()].contiguous()
+    _, part = fp8(g2, w.with_(M=123))
+    assert np.array_equal(part, full[:, perm])
+
+
+def test_train_outputs_do_not_depend_on_test_rows(thr):
+    w, x, g = thr
+    tr_full, _ = fp8(g, w)
+    g0 = dict(g)
+    g0["q_test"] = None
+    tr_only, te_only = fp8(g0, w.with_(M=0))
+    assert te_only.shape[1] == 0
+    assert np.array_equal(tr_full, tr_only)
+
+
+def test_test_rows_equal_to_train_rows_give_identical_outputs(thr):
+    w, x, g = thr
+    g2 = dict(g)
+    g2["q_test"] = g["q_train"][:, 100:300].contiguous()
+    tr, te = fp8(g2, w.with_(M=200))
+    assert np.array_equal(te, tr[:, 100:300])
+
+
+def test_determinism_prequantized_and_bf16_output(thr):
+    w, x, g = thr
+    a_tr, a_te = fp8(g, w)
+    b_tr, b_te = fp8(g, w)
+    assert np.array_equal(a_tr, b_tr) and np.array_equal(a_te, b_te)
+    qz = tfm.tfm_quantize_qkv_per_head(g["q_train"], g["k"], g["v"], g["q_test"])
+    p_tr, p_te = tfm.tfm_icl_attention_fp8_prequantized(qz["q8_train"], qz["k8"], qz["v8"], qz["q8_test"],
+                                                        qz["s_q"], qz["s_k"], qz["s_v"], alpha=w.alpha)
+    assert np.array_equal(p_tr.cpu().numpy(), a_tr) and np.array_equal(p_te.cpu().numpy(), a_te)
+    h_tr, h_te = fp8(g, w, out_dtype=torch.bfloat16)
+    assert np.array_equal(h_tr, torch.from_numpy(a_tr).to(torch.bfloat16).float().numpy())
+    assert np.array_equal(h_te, torch.from_numpy(a_te).to(torch.bfloat16).float().numpy())
+
+
+def test_train_row_permutation(thr):
+    # Permuting the train rows permutes the codes exactly.  The outputs change only
+    # through the key-tile order of the P rounding, so both orders stay within T2.
+    w, x, g = thr
+    perm = torch.from_numpy(np.random.default_rng(23).permutation(w.N)).cuda()
+    g2 = {"q_train": g["q_train"][:, perm].contiguous(), "k": g["k"][:, perm].contiguous(),
+          "v": g["v"][:, perm].contiguous(), "q_test": g["q_test"]}
+    a = tfm.tfm_quantize_qkv_per_head(g["q_train"], g["k"], g["v"], g["q_test"])
+    p = tfm.tfm_quantize_qkv_per_head(g2["q_train"], g2["k"], g2["v"], g2["q_test"])
+    for key in ("q8_train", "k8", "v8"):
+        assert torch.equal(p[key], a[key][:, :, perm])
+    assert torch.equal(p["q8_test"], a["q8_test"])
+    b_tr, b_te = fp8(g2, w)
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    pc = perm.cpu().numpy()
+    rows = sample_rows(w.N, 32, 24)
+    for b in range(w.B):
+        for h in range(w.H):
+            assert_t2(b_tr[b, rows, h], qz, w.alpha, b, h, qz["q8_train"][b, h, pc[rows]])
+            assert_t2(b_te[b, :32, h], qz, w.alpha, b, h, qz["q8_test"][b, h, :32])
+
+
+# ---------------- bf16 baseline ----------------
+
+def bf16_bound(q, k, v, alpha):
+    """Elementwise bound on |O_bf16 - O| from rounding P to bf16 for the PV product.
+
+    The kernel normalises by the fp32 row sum of the unrounded weights p_j, so
+    O_bf16 - O = sum_j (w_j - p_j) v_j / sum_j p_j with |w_j - p_j| <= 2^-8 p_j
+    (half a bf16 ulp)."""
+    s = alpha * (q @ k.T)
+    p = np.exp(s - s.max(axis=1, keepdims=True))
+    o = (p @ v) / p.sum(axis=1, keepdims=True)
+    return o, (2.0 ** -8 * p) @ np.abs(v) / p.sum(axis=1)[:, None]
+
+
+@pytest.mark.parametrize("name,B,H,D,N,M", [("tiny", 1, 2, 64, 512, 128), ("edge", 1, 2, 64, 65, 3),
+                                            ("edge", 2, 1, 128, 300, 50), ("threshold", 1, 6, 64, 8192, 2048)])
+def test_bf16_kernel_against_exact_attention(name, B, H, D, N, M):
+    w = WORKLOADS.get(name, Workload(name, B=B, H=H, D=D, N=N, M=M, dtype="bf16", seed=N)).with_(dtype="bf16")
+    x = generate(w)
+    g = gpu_inputs(x, torch.bfloat16)
+    o_tr, o_te = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    o_tr, o_te = o_tr.cpu().numpy(), o_te.cpu().numpy()
+    rt, re = sample_rows(w.N, 64, 9), sample_rows(w.M, 32, 10)
+    for b in range(w.B):
+        for h in range(w.H):
+            for o, q, rows in ((o_tr, x["q_train"], rt), (o_te, x["q_test"], re)):
+                ref, bnd = bf16_bound(q[b, rows, h].astype(np.float64), x["k"][b, :, h].astype(np.float64),
+                                      x["v"][b, :, h].astype(np.float64), w.alpha)
+                rms = np.sqrt(np.mean(ref ** 2))
+                err = np.abs(o[b, rows, h] - ref)
+                assert np.all(err <= 1.25 * bnd + 1e-5 * rms), (err / (bnd + 1e-30)).max()
+
+
+def test_bf16_kernel_invariances(thr):
+    w, x, g = thr
+    a = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    b = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], None, alpha=w.alpha)
+    c = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha, out_dtype=torch.bfloat16)
+    assert torch.equal(a[0], b[0])
+    assert torch.equal(c[0], a[0].to(torch.bfloat16)) and torch.equal(c[1], a[1].to(torch.bfloat16))

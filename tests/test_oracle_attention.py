@@ -162,3 +162,32 @@ def test_lift_keeps_subnormal_weights():
     w = A.one_pass_fp8_attention(q8, k8, np.eye(2), 17.5 / 32.0, 1.0, 64)[0]
     assert w[1] == 2.0 ** -9 / (256.0 + 2.0 ** -9)
     assert w[0] == 256.0 / (256.0 + 2.0 ** -9)
+
+
+def test_tie_allowance_bounds_the_effect_of_perturbed_exponents():
+    # With a single key tile the output depends on c only through the e4m3
+    # rounding of P~ (the lifted weights are normalised by their own sum), so it
+    # is piecewise constant in c.  Moving c by a relative amount that moves every
+    # P~ by less than tie_rel can only flip the rounding of P~ values inside the
+    # tie window, so the result moves by at most the returned allowance.
+    rng = np.random.default_rng(25)
+    N, D = 700, 64
+    q8 = decode(encode_rne(np.clip(rng.standard_normal((40, D)) * 80, -448, 448)))
+    k8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 80, -448, 448)))
+    v8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 80, -448, 448)))
+    c = 1.3e-5
+    o, allow = A.one_pass_fp8_attention(q8, k8, v8, c, 0.01, N, tie_rel=1e-4)
+    assert np.array_equal(o, A.one_pass_fp8_attention(q8, k8, v8, c, 0.01, N))
+    assert allow.max() > 0
+    # relative move of P~ = 2^(c f (s - m) + 8) is (2^((f-1) c |s - m|) - 1) <= 1e-4 here
+    span = c * np.max((q8 @ k8.T).max(axis=1) - (q8 @ k8.T).min(axis=1))
+    moved = 0
+    for f in (1 + 0.9e-4 / span, 1 - 0.9e-4 / span, 1 + 0.3e-4 / span):
+        o2 = A.one_pass_fp8_attention(q8, k8, v8, c * f, 0.01, N)
+        d = np.abs(o2 - o)
+        moved += np.count_nonzero(d > 1e-12 * np.abs(o).max())
+        assert np.all(d <= allow * 1.001 + 1e-12 * np.abs(o).max())
+    assert moved > 0
+    # with a tiny window nothing is flagged in a generic row
+    _, allow0 = A.one_pass_fp8_attention(q8[:3], k8, v8, c, 0.01, N, tie_rel=1e-15)
+    assert allow0.max() < 1e-9 * np.abs(o).max()
