@@ -79,15 +79,45 @@ def cpu_baseline(x, w, rows):
             "seconds": round(t_attn, 2)}
 
 
+def time_sdpa(g, w, steps, warmup):
+    """torch SDPA (flash backend only), the two ICL calls as two calls: context, not the baseline."""
+    import torch
+    from torch.nn.attention import SDPBackend, sdpa_kernel
+    F = torch.nn.functional
+    to_bhsd = lambda t: t.to(torch.bfloat16).transpose(1, 2).contiguous()
+    q_tr, k, v, q_te = (to_bhsd(g[n]) for n in ("q_train", "k", "v", "q_test"))
+    try:
+        with sdpa_kernel([SDPBackend.FLASH_ATTENTION]):
+            run = lambda: (F.scaled_dot_product_attention(q_tr, k, v, scale=w.alpha),
+                           F.scaled_dot_product_attention(q_te, k, v, scale=w.alpha))
+            for _ in range(warmup):
+                run()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(steps):
+                run()
+            e1.record()
+            torch.cuda.synchronize()
+    except RuntimeError as e:
+        log("sdpa flash backend unavailable:", str(e)[:200])
+        return None
+    ms = e0.elapsed_time(e1) / steps
+    log("torch sdpa (flash) %.3f ms" % ms)
+    return {"ms": round(ms, 4), "tflops": round(w.flops / ms / 1e9, 2), "backend": "flash"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mid")
-    ap.add_argument("--cpu-rows", type=int, default=1024, help="query rows of the oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=8192, help="query rows of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-bf16", action="store_true")
+    ap.add_argument("--sdpa", action="store_true",
+                    help="also time torch's scaled_dot_product_attention (flash backend, bf16) as context")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (for scaling HBM counters)")
     args = ap.parse_args()
@@ -171,6 +201,10 @@ def main():
         bf16 = {"ms": round(bf16_ms, 4), "tflops": round(w.flops / bf16_ms / 1e9, 2)}
         log("bf16 %.3f ms" % bf16_ms)
 
+    sdpa = None
+    if args.sdpa:
+        sdpa = time_sdpa(g, w, K, args.warmup)
+
     if args.copy_calibration:
         a = torch.empty(1 << 30, dtype=torch.uint8, device=dev)
         b = torch.empty_like(a)
@@ -194,6 +228,7 @@ def main():
         "speedup_vs_bf16": round(bf16["ms"] / ms_step, 3) if bf16 else None,
         "attention_only_speedup_vs_bf16": round(bf16["ms"] / attn_ms, 3) if bf16 else None,
         "bf16": bf16,
+        "torch_sdpa_bf16_context": sdpa,
         "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": traffic},

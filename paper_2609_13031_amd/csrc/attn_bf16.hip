@@ -1,21 +1,35 @@
 // bf16 ICL attention on gfx950: the 16-bit baseline built in the same library.
 //
 // The same two ICL calls as the FP8 kernel (N train + M test query rows of
-// each (b, h) against the same N train keys/values, Eq. (1) of the paper),
-// the same tiling (4 wave64s x 32 query rows, 64-key tiles through LDS) and
-// the same one-pass fp32 online softmax in the exp2 domain, without any
-// quantization: S^T = K Q^T and O^T += V^T P^T with
-// v_mfma_f32_32x32x16_bf16, P rounded to bf16 (round to nearest even) for
-// the PV product and l summed from the fp32 P.  The bf16 inputs are read in
-// their (B, rows, H, D) layout; the V tile is transposed while it is written
-// to LDS, with its keys in the row order of the QK^T accumulator.
+// each (b, h) against the same N train keys/values, Eq. (1) of the paper)
+// with the same structure, without quantization:
+//  * a workgroup of 4 wave64s owns 128 query rows of one (b, h); 32 per wave;
+//  * key blocks of kBlockKvBf16 keys; K and V are staged through LDS in their
+//    row-major bf16 layout (double-buffered, one barrier per block);
+//  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds the scores
+//    of one query row;
+//  * one-pass online softmax in fp32 in the exp2 domain; the running state is
+//    rescaled only on blocks where some row's max grew;
+//  * P is rounded to bf16 (round to nearest even) and is directly the B
+//    operand of O^T += V^T P^T (v_mfma_f32_32x32x16_bf16); the V^T operand is
+//    read from the row-major V tile with ds_read_b64_tr_b16, the transposing
+//    LDS read (in each 16-lane group, output lane i, element r is element i%4
+//    of the 4 that input lane 4r + i/4 addressed);
+//  * the row sum l = sum bf16(P) comes from v_mfma_f32_16x16x32_bf16 of a
+//    constant 0/1 operand against the same P operand, so the weights used in
+//    PV are normalised by their own sum.
 #include "common.h"
 
 namespace tfm {
 namespace {
 
 constexpr int kRowsPerBlock = 128;
-constexpr int kPadB = 16;  // bytes
+constexpr int kPadB = 16;        // bytes of LDS row padding
+constexpr int kBlockKvBf16 = 64;
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef float v8f __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 struct Bf16Args {
   int B, H, N, M, tiles;
@@ -28,30 +42,66 @@ struct Bf16Args {
   void* o_test;
 };
 
-typedef uint16_t v8u16 __attribute__((ext_vector_type(8)));
-typedef float v8f __attribute__((ext_vector_type(8)));
-
 __device__ inline v8bf as_bf(u32x4 w) {
   v8bf r;
   __builtin_memcpy(&r, &w, 16);
   return r;
 }
 
-// Position of key kk (0..63) in a transposed V tile row: the B operand of the
-// 32x32x16 PV product over keys [16q, 16q+16) holds, in lane half hf and
-// element e, key 16q + (e/4)*8 + hf*4 + e%4.
-__device__ inline int vt_pos(int kk) {
-  const int q = kk >> 4, kp = kk & 15;
-  const int hf = (kp >> 2) & 1, e = (kp >> 3) * 4 + (kp & 3);
-  return q * 16 + hf * 8 + e;
+__device__ inline v8bf cat_bf(v4s lo, v4s hi) {
+  v8bf r;
+  __builtin_memcpy(&r, &lo, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &hi, 8);
+  return r;
 }
 
-template <int D, bool OUT_BF16>
+__device__ inline v4s read_tr16(const uint8_t* lds_byte_ptr) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+      (lds_v4s*)((__attribute__((address_space(3))) uint8_t*)(lds_byte_ptr)));
+}
+
+__device__ inline float max_across_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Stage one block of K and V (BKV keys x D bf16 each, rows >= N as zero) into registers.
+template <int D, int BKV>
+__device__ inline void stage_load(const uint16_t* kb_ptr, const uint16_t* vb_ptr, int row_stride, int key0, int N,
+                                  u32x4* kr, u32x4* vr) {
+  constexpr int PIECES = BKV * D / 8 / 256;
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    const int r = i / (D / 8), cc = i % (D / 8);
+    const int key = key0 + r;
+    const size_t off = (size_t)key * row_stride + cc * 8;
+    kr[j] = key < N ? *reinterpret_cast<const u32x4*>(kb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
+    vr[j] = key < N ? *reinterpret_cast<const u32x4*>(vb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int D, int BKV>
+__device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* kr, const u32x4* vr) {
+  constexpr int RS = 2 * D + kPadB;
+  constexpr int PIECES = BKV * D / 8 / 256;
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    const int off = (i / (D / 8)) * RS + (i % (D / 8)) * 16;
+    *reinterpret_cast<u32x4*>(k_lds + off) = kr[j];
+    *reinterpret_cast<u32x4*>(v_lds + off) = vr[j];
+  }
+}
+
+template <int D, int BKV, bool OUT_BF16>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
-  constexpr int KS = 2 * D + kPadB;      // K tile row stride (bytes)
-  constexpr int VS = 2 * 64 + kPadB;     // V^T tile row stride (bytes)
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds[64 * KS];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds[D * VS];
+  constexpr int RS = 2 * D + kPadB;      // LDS row stride (bytes) of both tiles
+  constexpr int TBYTES = BKV * RS;
+  constexpr int NS = BKV / 32;           // 32-key score tiles
+  constexpr int NQ = BKV / 16;           // 16-key PV chunks
+  constexpr int PIECES = BKV * D / 8 / 256;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 2 * TBYTES];
 
   const int bh = blockIdx.x / a.tiles;
   const int tile = blockIdx.x % a.tiles;
@@ -73,101 +123,111 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   }
   const float c = a.alpha * kLog2e;
 
+  // constant operand of the row-sum MFMA: 1.0 in rows {0,8} for k-groups {0,2}
+  // and rows {4,12} for k-groups {1,3} (the lanes of one query in the P operand)
+  v8bf ones;
+  {
+    const int r16 = lane % 16, g = lane / 16;
+    const bool on = ((r16 == 0 || r16 == 8) && (g == 0 || g == 2)) || ((r16 == 4 || r16 == 12) && (g == 1 || g == 3));
+    const uint32_t w = on ? 0x3f803f80u : 0u;
+    ones = as_bf(u32x4{w, w, w, w});
+  }
+
   v16f acc_o[D / 32];
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) acc_o[i] = v16f{};
-  float l_run = 0.0f;
+  v4f lacc = v4f{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff();
 
-  const int ntiles = (N + 63) / 64;
-  for (int kt = 0; kt < ntiles; ++kt) {
-    __syncthreads();
-    // K tile: 64 keys x D bf16, row-major
-#pragma unroll
-    for (int i = threadIdx.x; i < 64 * D / 8; i += 256) {
-      const int r = i / (D / 8), cc = i % (D / 8);
-      const int key = kt * 64 + r;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (key < N) w = *reinterpret_cast<const u32x4*>(a.k + (((size_t)b * N + key) * H + h) * D + cc * 8);
-      *reinterpret_cast<u32x4*>(k_lds + r * KS + cc * 16) = w;
-    }
-    // V tile transposed: v_lds[d][pos(key)]
-#pragma unroll
-    for (int i = threadIdx.x; i < 64 * D / 8; i += 256) {
-      const int r = i % 64, cc = i / 64;
-      const int key = kt * 64 + r;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (key < N) w = *reinterpret_cast<const u32x4*>(a.v + (((size_t)b * N + key) * H + h) * D + cc * 8);
-      const int pos = vt_pos(r);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint16_t x = (uint16_t)(w[e / 2] >> (16 * (e % 2)));
-        *reinterpret_cast<uint16_t*>(v_lds + (cc * 8 + e) * VS + 2 * pos) = x;
-      }
-    }
-    __syncthreads();
+  const uint16_t* kb_ptr = a.k + ((size_t)b * N * H + h) * D;
+  const uint16_t* vb_ptr = a.v + ((size_t)b * N * H + h) * D;
+  const int row_stride = H * D;
+  const int nblocks = (N + BKV - 1) / BKV;
 
-    v16f s0 = v16f{}, s1 = v16f{};
+  // per-lane byte offsets of the transposing V reads (see the header comment):
+  // lane = 16g + 4r + j reads 4 consecutive d of key (g/2)*4 + r at d = 16(g%2) + 4j
+  const int tg = lane / 16, tr = (lane / 4) % 4, tj = lane % 4;
+  const int vtr_off = ((tg / 2) * 4 + tr) * RS + (16 * (tg % 2) + 4 * tj) * 2;
+
+  u32x4 kr[PIECES], vr[PIECES];
+  stage_load<D, BKV>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
+  stage_store<D, BKV>(lds, lds + TBYTES, kr, vr);
+  __syncthreads();
+
+  for (int kb = 0; kb < nblocks; ++kb) {
+    const uint8_t* k_lds = lds + (kb & 1) * 2 * TBYTES;
+    const uint8_t* v_lds = k_lds + TBYTES;
+    const bool more = kb + 1 < nblocks;
+    if (more) stage_load<D, BKV>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
+
+    v16f st[NS];
 #pragma unroll
-    for (int j = 0; j < D / 16; ++j) {
-      v8bf k0 = as_bf(*reinterpret_cast<const u32x4*>(k_lds + ql * KS + 32 * j + 16 * half));
-      v8bf k1 = as_bf(*reinterpret_cast<const u32x4*>(k_lds + (32 + ql) * KS + 32 * j + 16 * half));
-      s0 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k0, qf[j], s0, 0, 0, 0);
-      s1 = __builtin_amdgcn_mfma_f32_32x32x16_bf16(k1, qf[j], s1, 0, 0, 0);
-    }
-    if (kt * 64 + 64 > N) {
+    for (int t = 0; t < NS; ++t) {
+      st[t] = v16f{};
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt * 64 + (r / 4) * 8 + half * 4 + (r % 4);
-        if (key >= N) s0[r] = -__builtin_inff();
-        if (key + 32 >= N) s1[r] = -__builtin_inff();
+      for (int j = 0; j < D / 16; ++j) {
+        v8bf kf = as_bf(*reinterpret_cast<const u32x4*>(k_lds + (32 * t + ql) * RS + 32 * j + 16 * half));
+        st[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[j], st[t], 0, 0, 0);
       }
     }
-    float mx = s0[0];
+    if (kb * BKV + BKV > N) {
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s0[r]);
+      for (int t = 0; t < NS; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s1[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+        for (int r = 0; r < 16; ++r)
+          if (kb * BKV + 32 * t + (r / 4) * 8 + half * 4 + (r % 4) >= N) st[t][r] = -__builtin_inff();
+    }
+
+    float mx = st[0][0];
+#pragma unroll
+    for (int t = 0; t < NS; ++t)
+#pragma unroll
+      for (int r = (t == 0 ? 1 : 0); r < 16; ++r) mx = fmaxf(mx, st[t][r]);
+    mx = max_across_halves(mx);
     const float m_new = fmaxf(m_run, mx);
     const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));
     const float bias = -c * m_new;
     m_run = m_new;
 
-    float lsum = 0.0f;
+    // P in bf16, 16-key chunk q = accumulator rows [8(q%2), +8) of score tile q/2
+    v8bf pf[NQ];
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      s0[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s0[r], c, bias));
-      s1[r] = __builtin_amdgcn_exp2f(__builtin_fmaf(s1[r], c, bias));
-      lsum += s0[r] + s1[r];
-    }
-    lsum += __shfl_xor(lsum, 32);
-    l_run = l_run * rescale + lsum;
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i) acc_o[i] *= rescale;
-
-    // P fragments: chunk q covers keys [16q, 16q+16) = accumulator rows 8(q%2).. of s0 (q<2) / s1
-    v8bf pfr[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const v16f& src = q < 2 ? s0 : s1;
+    for (int q = 0; q < NQ; ++q) {
+      const v16f& src = st[q / 2];
       v8f pv;
 #pragma unroll
-      for (int e = 0; e < 8; ++e) pv[e] = src[8 * (q % 2) + e];
-      pfr[q] = __builtin_convertvector(pv, v8bf);
+      for (int e = 0; e < 8; ++e) pv[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(src[8 * (q % 2) + e], c, bias));
+      pf[q] = __builtin_convertvector(pv, v8bf);
+    }
+
+    if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc_o[i][j] = acc_o[i][j] * rescale;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lacc[j] = lacc[j] * rescale;
     }
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) {
+    for (int q = 0; q < NQ; ++q) {
+      lacc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[q], lacc, 0, 0, 0);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        v8bf va = as_bf(*reinterpret_cast<const u32x4*>(v_lds + (32 * i + ql) * VS + 2 * (16 * q + 8 * half)));
-        acc_o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pfr[q], acc_o[i], 0, 0, 0);
+      for (int i = 0; i < D / 32; ++i) {
+        const uint8_t* base = v_lds + (16 * q) * RS + 64 * i + vtr_off;
+        const v8bf va = cat_bf(read_tr16(base), read_tr16(base + 8 * RS));
+        acc_o[i] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va, pf[q], acc_o[i], 0, 0, 0);
       }
     }
+
+    if (more) {
+      uint8_t* nk = lds + ((kb + 1) & 1) * 2 * TBYTES;
+      stage_store<D, BKV>(nk, nk + TBYTES, kr, vr);
+    }
+    __syncthreads();
   }
 
   if (row >= N + M) return;
-  const float inv = 1.0f / l_run;
+  const float inv = 1.0f / lacc[0];
   const size_t orow = row < N ? (((size_t)b * N + row) * H + h) * D : (((size_t)b * M + (row - N)) * H + h) * D;
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) {
@@ -202,11 +262,11 @@ hipError_t launch_attn_bf16(int out_bf16, int B, int H, int D, int N, int M, flo
   a.o_train = o_train; a.o_test = o_test;
   dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
   if (D == 64) {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, false>), grid, block, 0, s, a);
   } else {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -55,13 +55,62 @@ __device__ inline v4f mfma_f8_16x16x128(v8i a, v8i b, v4f c) {
   return __builtin_amdgcn_mfma_scale_f32_16x16x128_f8f6f4(a, b, c, 0, 0, 0, 0, 0, 0);
 }
 
-template <int D, bool OUT_BF16>
+// Max of x over the 64 lanes' two halves (lanes l and l+32 hold the same query).
+__device__ inline float max_across_halves(float x) {
+  auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+
+// Four P~ values rounded to e4m3 and packed little-endian into one dword.
+__device__ inline int pack4_e4m3(float p0, float p1, float p2, float p3) {
+  // the first conversion fills the low half; its high half is overwritten by the second
+  const int lo = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, __float_as_int(p0), false);
+  return __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, lo, true);
+}
+
+// Stage one key block (BKV keys) of K (row-major, rows >= N read as zero) and
+// V^T (BKV/64 tiles of D x 64 bytes, tiles past the end read as zero) into
+// registers, 16 bytes per thread per piece.
+template <int D, int BKV>
+__device__ inline void stage_load(const uint8_t* kbase, const uint8_t* vbase, int kb, int N, int ntiles64,
+                                  u32x4* kr, u32x4* vr) {
+  constexpr int PIECES = BKV * D / 16 / 256;
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    const int r = i / (D / 16), cc = i % (D / 16);
+    const int key = kb * BKV + r;
+    kr[j] = key < N ? *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16) : u32x4{0u, 0u, 0u, 0u};
+    const int t64 = kb * (BKV / 64) + i / (D * 4);          // 64-key tile of this piece
+    vr[j] = t64 < ntiles64 ? *reinterpret_cast<const u32x4*>(vbase + (size_t)t64 * D * 64 + (i % (D * 4)) * 16)
+                           : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+template <int D, int BKV>
+__device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* kr, const u32x4* vr) {
+  constexpr int KS = D + kPad, VS = 64 + kPad;
+  constexpr int PIECES = BKV * D / 16 / 256;
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    const int i = threadIdx.x + 256 * j;
+    *reinterpret_cast<u32x4*>(k_lds + (i / (D / 16)) * KS + (i % (D / 16)) * 16) = kr[j];
+    // V^T tiles stacked: row (tile*D + d) of 64 bytes
+    *reinterpret_cast<u32x4*>(v_lds + (i / 4) * VS + (i % 4) * 16) = vr[j];
+  }
+}
+
+template <int D, int BKV, bool OUT_BF16>
 __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   constexpr int KD = D / 64;            // 64-wide head_dim chunks (k of one MFMA)
-  constexpr int KS = D + kPad;          // K tile row stride in LDS
-  constexpr int VS = 64 + kPad;         // V^T tile row stride in LDS
-  __shared__ __attribute__((aligned(16))) uint8_t k_lds[64 * KS];
-  __shared__ __attribute__((aligned(16))) uint8_t v_lds[D * VS];
+  constexpr int NS = BKV / 32;          // 32-key score tiles per key block
+  constexpr int NP = BKV / 64;          // 64-key PV chunks per key block
+  constexpr int KS = D + kPad;          // K row stride in LDS
+  constexpr int VS = 64 + kPad;         // V^T row stride in LDS
+  constexpr int KBYTES = BKV * KS, VBYTES = NP * D * VS;
+  constexpr int PIECES = BKV * D / 16 / 256;
+  // two K/V stages: the next key block is written while the current one is read
+  __shared__ __attribute__((aligned(16))) uint8_t lds[2 * (KBYTES + VBYTES)];
 
   const int bh = blockIdx.x / a.tiles;
   const int tile = blockIdx.x % a.tiles;
@@ -98,79 +147,90 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   v4f lacc = v4f{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff();
 
-  const int ntiles = (N + 63) / 64;
+  const int ntiles64 = (N + 63) / 64;
+  const int nblocks = (N + BKV - 1) / BKV;
   const uint8_t* kbase = a.k8 + (size_t)bh * N * D;
-  const uint8_t* vbase = a.v8t + (size_t)bh * ntiles * D * 64;
+  const uint8_t* vbase = a.v8t + (size_t)bh * ntiles64 * D * 64;
 
-  for (int kt = 0; kt < ntiles; ++kt) {
-    // ---- stage K (64 x D, row-major) and V^T (D x 64) tiles into LDS ----
-    __syncthreads();
-#pragma unroll
-    for (int i = threadIdx.x; i < 64 * D / 16; i += 256) {
-      const int r = i / (D / 16), cc = i % (D / 16);
-      const int key = kt * 64 + r;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (key < N) w = *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16);
-      *reinterpret_cast<u32x4*>(k_lds + r * KS + cc * 16) = w;
-    }
-#pragma unroll
-    for (int i = threadIdx.x; i < D * 4; i += 256) {
-      const int r = i / 4, cc = i % 4;
-      u32x4 w = *reinterpret_cast<const u32x4*>(vbase + (size_t)kt * D * 64 + r * 64 + cc * 16);
-      *reinterpret_cast<u32x4*>(v_lds + r * VS + cc * 16) = w;
-    }
-    __syncthreads();
+  u32x4 kr[PIECES], vr[PIECES];
+  stage_load<D, BKV>(kbase, vbase, 0, N, ntiles64, kr, vr);
+  stage_store<D, BKV>(lds, lds + KBYTES, kr, vr);
+  __syncthreads();
 
-    // ---- S^T = K_8 Q_8^T for the two 32-key halves ----
-    v16f s0 = v16f{}, s1 = v16f{};
+  for (int kb = 0; kb < nblocks; ++kb) {
+    uint8_t* k_lds = lds + (kb & 1) * (KBYTES + VBYTES);
+    uint8_t* v_lds = k_lds + KBYTES;
+    const bool more = kb + 1 < nblocks;
+    if (more) stage_load<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
+
+    // ---- S^T = K_8 Q_8^T, 32 keys per accumulator tile ----
+    v16f st[NS];
 #pragma unroll
-    for (int s = 0; s < KD; ++s) {
-      s0 = mfma_f8_32x32x64(load32(k_lds + ql * KS + 64 * s + 32 * half), qf[s], s0);
-      s1 = mfma_f8_32x32x64(load32(k_lds + (32 + ql) * KS + 64 * s + 32 * half), qf[s], s1);
+    for (int t = 0; t < NS; ++t) {
+      st[t] = v16f{};
+#pragma unroll
+      for (int s = 0; s < KD; ++s) st[t] = mfma_f8_32x32x64(load32(k_lds + (32 * t + ql) * KS + 64 * s + 32 * half), qf[s], st[t]);
     }
-    // keys beyond N (last tile only) take no part
-    if (kt * 64 + 64 > N) {
+    // keys beyond N (last block only) take no part
+    if (kb * BKV + BKV > N) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt * 64 + (r / 4) * 8 + half * 4 + (r % 4);
-        if (key >= N) s0[r] = -__builtin_inff();
-        if (key + 32 >= N) s1[r] = -__builtin_inff();
-      }
+      for (int t = 0; t < NS; ++t)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          if (kb * BKV + 32 * t + (r / 4) * 8 + half * 4 + (r % 4) >= N) st[t][r] = -__builtin_inff();
     }
 
-    // ---- online softmax in the exp2 domain ----
-    float mx = s0[0];
+    // ---- running max over the block; rescale the state by 2^(c (m_old - m_new)) ----
+    float mx = st[0][0];
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s0[r]);
+    for (int t = 0; t < NS; ++t)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s1[r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+      for (int r = (t == 0 ? 1 : 0); r < 16; ++r) mx = fmaxf(mx, st[t][r]);
+    mx = max_across_halves(mx);
     const float m_new = fmaxf(m_run, mx);
-    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 0 on the first tile
+    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 1 where unchanged, 0 at the start
     const float bias = 8.0f - c * m_new;                                   // lifts the running max to 2^8
     m_run = m_new;
 
-    v8i pf;
+    // ---- P~ = 2^(c S + bias) rounded to e4m3, directly the B operand of the PV product ----
+    v8i pf[NP];
 #pragma unroll
-    for (int w = 0; w < 8; ++w) {
-      const v16f& src = w < 4 ? s0 : s1;
-      const int r = 4 * (w % 4);
-      const float p0 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 0], c, bias));
-      const float p1 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 1], c, bias));
-      const float p2 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 2], c, bias));
-      const float p3 = __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 3], c, bias));
-      int lo = __builtin_amdgcn_cvt_pk_fp8_f32(p0, p1, 0, false);
-      pf[w] = __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, lo, true);
+    for (int p = 0; p < NP; ++p)
+#pragma unroll
+      for (int w = 0; w < 8; ++w) {
+        const v16f& src = st[2 * p + w / 4];
+        const int r = 4 * (w % 4);
+        pf[p][w] = pack4_e4m3(__builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 0], c, bias)),
+                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 1], c, bias)),
+                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 2], c, bias)),
+                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 3], c, bias)));
+      }
+
+    // ---- l += sum P_8 (row-sum MFMA) and O^T += V_8^T P_8^T ----
+    // Rescale the running state only when some row's max grew (rescale is exactly
+    // 1 where it did not).  Written element-wise so the accumulators are scaled in
+    // place inside the wave-uniform branch.
+    if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) acc_o[i][j] = acc_o[i][j] * rescale;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) lacc[j] = lacc[j] * rescale;
+    }
+#pragma unroll
+    for (int p = 0; p < NP; ++p) {
+      lacc = mfma_f8_16x16x128(ones, pf[p], lacc);
+#pragma unroll
+      for (int i = 0; i < D / 32; ++i)
+        acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (p * D + 32 * i + ql) * VS + 32 * half), pf[p], acc_o[i]);
     }
 
-    // ---- rescale the running state, then accumulate l and O^T ----
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i) acc_o[i] *= rescale;
-    lacc *= rescale;
-    lacc = mfma_f8_16x16x128(ones, pf, lacc);
-#pragma unroll
-    for (int i = 0; i < D / 32; ++i)
-      acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (32 * i + ql) * VS + 32 * half), pf, acc_o[i]);
+    if (more) {
+      uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
+      stage_store<D, BKV>(nk, nk + KBYTES, kr, vr);
+    }
+    __syncthreads();
   }
 
   // ---- epilogue: O * s_v / l ----
@@ -210,11 +270,11 @@ hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, floa
   a.s_q = s_q; a.s_k = s_k; a.s_v = s_v; a.o_train = o_train; a.o_test = o_test;
   dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
   if (D == 64) {
-    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_fp8_kernel<64, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, false>), grid, block, 0, s, a);
   } else {
-    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_fp8_kernel<128, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

@@ -14,7 +14,10 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
-constexpr int kBlockKv = 64;          // keys per tile of both attention kernels
+#ifndef TFM_FP8_BLOCK_KV
+#define TFM_FP8_BLOCK_KV 128
+#endif
+constexpr int kBlockKv = TFM_FP8_BLOCK_KV;  // keys per block (running-max granularity) of the FP8 kernel
 constexpr float kLog2e = 1.4426950408889634f;
 
 // Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).

@@ -36,8 +36,8 @@ def test_status_strings_and_version():
 
 
 def test_block_kv_and_workspace_queries():
-    assert tfm.tfm_icl_attention_fp8_block_kv(64) == 64
-    assert tfm.tfm_icl_attention_fp8_block_kv(128) == 64
+    assert tfm.tfm_icl_attention_fp8_block_kv(64) == 128
+    assert tfm.tfm_icl_attention_fp8_block_kv(128) == 128
     assert tfm.tfm_icl_attention_fp8_block_kv(96) == 0
     assert tfm.tfm_quantize_workspace_bytes(2, 6) == 512
     assert tfm.tfm_quantize_workspace_bytes(0, 6) == 0

@@ -18,7 +18,11 @@ from parity import (EPS_ACC, EPS_DOT, TIE_REL, assert_t1, assert_t1p, assert_t2,
                     sample_rows)
 
 pytestmark = pytest.mark.gpu
-BKV = 64
+BKV = 128   # keys per block of the FP8 kernel: the running-max granularity the oracle replays
+
+
+def test_library_block_size_is_the_one_the_oracle_replays():
+    assert tfm.tfm_icl_attention_fp8_block_kv(64) == BKV and tfm.tfm_icl_attention_fp8_block_kv(128) == BKV
 
 
 def fp8(g, w, out_dtype=torch.float32):
@@ -218,13 +222,14 @@ def test_train_row_permutation(thr):
 def bf16_bound(q, k, v, alpha):
     """Elementwise bound on |O_bf16 - O| from rounding P to bf16 for the PV product.
 
-    The kernel normalises by the fp32 row sum of the unrounded weights p_j, so
-    O_bf16 - O = sum_j (w_j - p_j) v_j / sum_j p_j with |w_j - p_j| <= 2^-8 p_j
-    (half a bf16 ulp)."""
+    The kernel normalises by the sum of the rounded weights w_j (a row-sum
+    MFMA over the same bf16 P), so O_bf16 - O = sum_j (w_j - p_j)(v_j - O) / sum_j w_j
+    with |w_j - p_j| <= 2^-8 p_j (half a bf16 ulp)."""
     s = alpha * (q @ k.T)
     p = np.exp(s - s.max(axis=1, keepdims=True))
     o = (p @ v) / p.sum(axis=1, keepdims=True)
-    return o, (2.0 ** -8 * p) @ np.abs(v) / p.sum(axis=1)[:, None]
+    num = np.stack([np.einsum("rj,rj->r", p, np.abs(v[None, :, c] - o[:, c][:, None])) for c in range(v.shape[1])], 1)
+    return o, 2.0 ** -8 * num / ((1 - 2.0 ** -8) * p.sum(axis=1))[:, None]
 
 
 @pytest.mark.parametrize("name,B,H,D,N,M", [("tiny", 1, 2, 64, 512, 128), ("edge", 1, 2, 64, 65, 3),
