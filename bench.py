@@ -107,6 +107,50 @@ def time_sdpa(g, w, steps, warmup):
     return {"ms": round(ms, 4), "tflops": round(w.flops / ms / 1e9, 2), "backend": "flash"}
 
 
+def crossover(max_n):
+    """FP8 vs bf16 for a single train-train call (B=1, H=8, M=0, bf16 in/out), the shape of the
+    paper's kernel tables, on synthetic tables drawn like the headline workload."""
+    import torch
+    from paper_2609_13031_amd import tfm
+    from paper_2609_13031_amd.workloads import Workload, generate
+
+    rows = []
+    for D in (64, 128):
+        N = 1024
+        while N <= max_n:
+            w = Workload("crossover", B=1, H=8, D=D, N=N, M=0, dtype="bf16", seed=N + D)
+            g = {k: torch.from_numpy(v).to(torch.bfloat16).cuda() for k, v in generate(w).items() if k != "q_test"}
+            o = torch.empty((1, N, 8, D), dtype=torch.bfloat16, device="cuda")
+            ws = torch.empty(tfm.tfm_icl_attention_fp8_workspace_bytes(1, 8, D, N, 0), dtype=torch.uint8,
+                             device="cuda")
+            reps = max(3, min(50, int(2e12 / w.flops)))
+            runs = {
+                "fp8": lambda: tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], None, alpha=w.alpha,
+                                                         out_dtype=torch.bfloat16, out=(o, None), workspace=ws),
+                "bf16": lambda: tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], None, alpha=w.alpha,
+                                                           out_dtype=torch.bfloat16, out=(o, None)),
+            }
+            res = {"D": D, "N": N}
+            for name, fn in runs.items():
+                fn()
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                for _ in range(reps):
+                    fn()
+                e1.record()
+                torch.cuda.synchronize()
+                res[name + "_ms"] = round(e0.elapsed_time(e1) / reps, 4)
+            res["fp8_tflops"] = round(w.flops / res["fp8_ms"] / 1e9, 1)
+            res["bf16_tflops"] = round(w.flops / res["bf16_ms"] / 1e9, 1)
+            res["speedup"] = round(res["bf16_ms"] / res["fp8_ms"], 3)
+            log("crossover", res)
+            rows.append(res)
+            del g, o, ws
+            N *= 2
+    return {"crossover": rows, "call": "train-train only, B=1, H=8, bf16 in/out, FP8 time includes quantization"}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -118,6 +162,10 @@ def main():
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--sdpa", action="store_true",
                     help="also time torch's scaled_dot_product_attention (flash backend, bf16) as context")
+    ap.add_argument("--crossover", action="store_true",
+                    help="instead of the headline step: FP8 (quantization included) vs bf16 for one train-train "
+                         "call, B=1, H=8, N=1k..512k, D=64 and 128; prints one JSON line with the table")
+    ap.add_argument("--crossover-max-n", type=int, default=1 << 19)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (for scaling HBM counters)")
     args = ap.parse_args()
@@ -133,6 +181,9 @@ def main():
     from paper_2609_13031_amd.workloads import WORKLOADS, generate
 
     tfm.lib()
+    if args.crossover:
+        print(json.dumps(crossover(args.crossover_max_n)), flush=True)
+        return
     w = WORKLOADS[args.workload]
     log("generating", w)
     x = generate(w)

@@ -168,17 +168,35 @@ int tfm_icl_attention_fp8_block_kv(int D);
 
 /*
  * tfm_icl_attention_bf16 -- the 16-bit baseline of the same two ICL calls
- * (Eq. (1), no quantization): bf16 Q/K/V, fp32 online softmax in one pass,
- * P rounded to bf16 for the PV product, fp32 accumulation.
+ * (Eq. (1), no quantization): bf16 Q/K/V (fp32 inputs are rounded to bf16 on
+ * load), fp32 online softmax in one pass, P rounded to bf16 for the PV
+ * product and normalised by the sum of the rounded P, fp32 accumulation.
  *
- *   q_train, k, v       (B, N, H, D) bf16;  q_test (B, M, H, D) bf16, NULL iff M == 0
+ *   in_dtype            TFM_BF16 or TFM_F32
+ *   q_train, k, v       (B, N, H, D);  q_test (B, M, H, D), NULL iff M == 0
  *   out_dtype           TFM_F32 or TFM_BF16
  *   o_train, o_test     as for tfm_icl_attention_fp8
  */
-int tfm_icl_attention_bf16(int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                           const void* q_train, const void* k, const void* v,
-                           const void* q_test, void* o_train, void* o_test,
-                           tfm_stream stream);
+int tfm_icl_attention_bf16(int in_dtype, int out_dtype, int B, int H, int D, int N, int M,
+                           float alpha, const void* q_train, const void* k, const void* v,
+                           const void* q_test, void* o_train, void* o_test, tfm_stream stream);
+
+/*
+ * tfm_icl_attention -- the paper's final configuration (Sec. 3, last
+ * paragraph; Sec. 4, "final configuration"): the FP8 path
+ * (tfm_icl_attention_fp8) when the table has more than `fp8_min_train_rows`
+ * train rows, where the quantization overhead is amortized, and the 16-bit
+ * path (tfm_icl_attention_bf16) otherwise.  fp8_min_train_rows < 0 selects
+ * the paper's gate of 8192 rows.  Arguments as for tfm_icl_attention_fp8;
+ * `used_fp8` (host memory, may be NULL) receives 1 if the FP8 path ran.
+ * The workspace is used only by the FP8 path.
+ */
+#define TFM_FP8_MIN_TRAIN_ROWS_DEFAULT 8192
+size_t tfm_icl_attention_workspace_bytes(int B, int H, int D, int N, int M, int fp8_min_train_rows);
+int tfm_icl_attention(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                      const void* q_train, const void* k, const void* v, const void* q_test,
+                      void* o_train, void* o_test, int fp8_min_train_rows, int* used_fp8,
+                      void* workspace, size_t workspace_bytes, tfm_stream stream);
 
 #ifdef __cplusplus
 }

@@ -209,17 +209,44 @@ int tfm_icl_attention_fp8_prequantized(int out_dtype, int B, int H, int D, int N
 
 int tfm_icl_attention_fp8_block_kv(int D) { return (D == 64 || D == 128) ? kBlockKv : 0; }
 
-int tfm_icl_attention_bf16(int out_dtype, int B, int H, int D, int N, int M, float alpha, const void* q_train,
-                           const void* k, const void* v, const void* q_test, void* o_train, void* o_test,
-                           tfm_stream stream) {
+int tfm_icl_attention_bf16(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                           const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
+                           void* o_test, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   TFM_TRY(check_alpha(alpha));
   const void* req[] = {q_train, k, v, o_train};
   const void* tst[] = {q_test, o_test};
   TFM_TRY(check_io(M > 0, req, 4, tst, 2));
-  return hip_status(launch_attn_bf16(out_dtype == TFM_BF16, B, H, D, N, M, alpha, q_train, q_test, k, v, o_train,
-                                     o_test, (hipStream_t)stream));
+  return hip_status(launch_attn_bf16(in_dtype == TFM_F32, out_dtype == TFM_BF16, B, H, D, N, M, alpha, q_train,
+                                     q_test, k, v, o_train, o_test, (hipStream_t)stream));
+}
+
+static int gate_rows(int fp8_min_train_rows) {
+  return fp8_min_train_rows < 0 ? TFM_FP8_MIN_TRAIN_ROWS_DEFAULT : fp8_min_train_rows;
+}
+
+size_t tfm_icl_attention_workspace_bytes(int B, int H, int D, int N, int M, int fp8_min_train_rows) {
+  if (check_shape(B, H, D, N, M) != TFM_OK) return 0;
+  return N > gate_rows(fp8_min_train_rows) ? fp8_workspace_layout(B, H, D, N, M).total : 0;
+}
+
+int tfm_icl_attention(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
+                      const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
+                      void* o_test, int fp8_min_train_rows, int* used_fp8, void* workspace, size_t workspace_bytes,
+                      tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  const bool fp8 = N > gate_rows(fp8_min_train_rows);
+  int st;
+  if (fp8)
+    st = tfm_icl_attention_fp8(in_dtype, out_dtype, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train, o_test,
+                               workspace, workspace_bytes, stream);
+  else
+    st = tfm_icl_attention_bf16(in_dtype, out_dtype, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train, o_test,
+                                stream);
+  if (st == TFM_OK && used_fp8) *used_fp8 = fp8 ? 1 : 0;
+  return st;
 }
 
 }  // extern "C"

@@ -28,19 +28,36 @@ constexpr int kPadB = 16;        // bytes of LDS row padding
 constexpr int kBlockKvBf16 = 64;
 
 typedef short v4s __attribute__((ext_vector_type(4)));
-typedef float v8f __attribute__((ext_vector_type(8)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 struct Bf16Args {
   int B, H, N, M, tiles;
   float alpha;
-  const uint16_t* q_train;
-  const uint16_t* q_test;
-  const uint16_t* k;
-  const uint16_t* v;
+  const void* q_train;
+  const void* q_test;
+  const void* k;
+  const void* v;
   void* o_train;
   void* o_test;
 };
+
+// Eight consecutive inputs as bf16 (fp32 inputs rounded to nearest even).
+template <typename T>
+__device__ inline u32x4 load8_as_bf16(const T* p) {
+  if constexpr (sizeof(T) == 2) {
+    return *reinterpret_cast<const u32x4*>(p);
+  } else {
+    const v4f lo = *reinterpret_cast<const v4f*>(p);
+    const v4f hi = *reinterpret_cast<const v4f*>(p + 4);
+    v8f x;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) { x[e] = lo[e]; x[4 + e] = hi[e]; }
+    const v8bf y = __builtin_convertvector(x, v8bf);
+    u32x4 r;
+    __builtin_memcpy(&r, &y, 16);
+    return r;
+  }
+}
 
 __device__ inline v8bf as_bf(u32x4 w) {
   v8bf r;
@@ -66,8 +83,8 @@ __device__ inline float max_across_halves(float x) {
 }
 
 // Stage one block of K and V (BKV keys x D bf16 each, rows >= N as zero) into registers.
-template <int D, int BKV>
-__device__ inline void stage_load(const uint16_t* kb_ptr, const uint16_t* vb_ptr, int row_stride, int key0, int N,
+template <int D, int BKV, typename T>
+__device__ inline void stage_load(const T* kb_ptr, const T* vb_ptr, int row_stride, int key0, int N,
                                   u32x4* kr, u32x4* vr) {
   constexpr int PIECES = BKV * D / 8 / 256;
 #pragma unroll
@@ -76,8 +93,8 @@ __device__ inline void stage_load(const uint16_t* kb_ptr, const uint16_t* vb_ptr
     const int r = i / (D / 8), cc = i % (D / 8);
     const int key = key0 + r;
     const size_t off = (size_t)key * row_stride + cc * 8;
-    kr[j] = key < N ? *reinterpret_cast<const u32x4*>(kb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
-    vr[j] = key < N ? *reinterpret_cast<const u32x4*>(vb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
+    kr[j] = key < N ? load8_as_bf16(kb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
+    vr[j] = key < N ? load8_as_bf16(vb_ptr + off) : u32x4{0u, 0u, 0u, 0u};
   }
 }
 
@@ -94,7 +111,7 @@ __device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* 
   }
 }
 
-template <int D, int BKV, bool OUT_BF16>
+template <int D, int BKV, typename T, bool OUT_BF16>
 __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   constexpr int RS = 2 * D + kPadB;      // LDS row stride (bytes) of both tiles
   constexpr int TBYTES = BKV * RS;
@@ -114,12 +131,12 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   // Q fragment: for head_dim chunk j (16 wide) the lane holds d in [16j + 8*half, +8)
   v8bf qf[D / 16];
   {
-    const uint16_t* qrow = nullptr;
-    if (row < N) qrow = a.q_train + (((size_t)b * N + row) * H + h) * D;
-    else if (row < N + M) qrow = a.q_test + (((size_t)b * M + (row - N)) * H + h) * D;
+    const T* qrow = nullptr;
+    if (row < N) qrow = (const T*)a.q_train + (((size_t)b * N + row) * H + h) * D;
+    else if (row < N + M) qrow = (const T*)a.q_test + (((size_t)b * M + (row - N)) * H + h) * D;
 #pragma unroll
     for (int j = 0; j < D / 16; ++j)
-      qf[j] = qrow ? as_bf(*reinterpret_cast<const u32x4*>(qrow + 16 * j + 8 * half)) : as_bf(u32x4{0u, 0u, 0u, 0u});
+      qf[j] = qrow ? as_bf(load8_as_bf16(qrow + 16 * j + 8 * half)) : as_bf(u32x4{0u, 0u, 0u, 0u});
   }
   const float c = a.alpha * kLog2e;
 
@@ -139,8 +156,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   v4f lacc = v4f{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff();
 
-  const uint16_t* kb_ptr = a.k + ((size_t)b * N * H + h) * D;
-  const uint16_t* vb_ptr = a.v + ((size_t)b * N * H + h) * D;
+  const T* kb_ptr = (const T*)a.k + ((size_t)b * N * H + h) * D;
+  const T* vb_ptr = (const T*)a.v + ((size_t)b * N * H + h) * D;
   const int row_stride = H * D;
   const int nblocks = (N + BKV - 1) / BKV;
 
@@ -150,7 +167,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   const int vtr_off = ((tg / 2) * 4 + tr) * RS + (16 * (tg % 2) + 4 * tj) * 2;
 
   u32x4 kr[PIECES], vr[PIECES];
-  stage_load<D, BKV>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
+  stage_load<D, BKV, T>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
   stage_store<D, BKV>(lds, lds + TBYTES, kr, vr);
   __syncthreads();
 
@@ -158,7 +175,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
     const uint8_t* k_lds = lds + (kb & 1) * 2 * TBYTES;
     const uint8_t* v_lds = k_lds + TBYTES;
     const bool more = kb + 1 < nblocks;
-    if (more) stage_load<D, BKV>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
+    if (more) stage_load<D, BKV, T>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
 
     v16f st[NS];
 #pragma unroll
@@ -250,24 +267,30 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
 
 }  // namespace
 
-hipError_t launch_attn_bf16(int out_bf16, int B, int H, int D, int N, int M, float alpha, const void* q_train,
-                            const void* q_test, const void* k, const void* v, void* o_train, void* o_test,
-                            hipStream_t s) {
+template <typename T>
+static void launch_bf16_typed(int out_bf16, int D, const Bf16Args& a, dim3 grid, hipStream_t s) {
+  dim3 block(256);
+  if (D == 64) {
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, false>), grid, block, 0, s, a);
+  } else {
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, false>), grid, block, 0, s, a);
+  }
+}
+
+hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, float alpha,
+                            const void* q_train, const void* q_test, const void* k, const void* v, void* o_train,
+                            void* o_test, hipStream_t s) {
   Bf16Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
   a.tiles = (N + M + kRowsPerBlock - 1) / kRowsPerBlock;
   a.alpha = alpha;
-  a.q_train = (const uint16_t*)q_train; a.q_test = (const uint16_t*)q_test;
-  a.k = (const uint16_t*)k; a.v = (const uint16_t*)v;
+  a.q_train = q_train; a.q_test = q_test; a.k = k; a.v = v;
   a.o_train = o_train; a.o_test = o_test;
-  dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
-  if (D == 64) {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, false>), grid, block, 0, s, a);
-  } else {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, false>), grid, block, 0, s, a);
-  }
+  dim3 grid((unsigned)((long)a.tiles * B * H));
+  if (in_f32) launch_bf16_typed<float>(out_bf16, D, a, grid, s);
+  else launch_bf16_typed<uint16_t>(out_bf16, D, a, grid, s);
   return hipGetLastError();
 }
 

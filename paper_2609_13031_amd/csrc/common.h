@@ -12,6 +12,7 @@ typedef int v8i __attribute__((ext_vector_type(8)));
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef float v8f __attribute__((ext_vector_type(8)));
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 #ifndef TFM_FP8_BLOCK_KV
@@ -57,8 +58,8 @@ hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, floa
                            const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8,
                            const uint8_t* v8t, const float* s_q, const float* s_k,
                            const float* s_v, void* o_train, void* o_test, hipStream_t s);
-// bf16 baseline attention over the N+M query rows of every (b,h).
-hipError_t launch_attn_bf16(int out_bf16, int B, int H, int D, int N, int M, float alpha,
+// bf16 baseline attention over the N+M query rows of every (b,h); fp32 inputs are rounded to bf16.
+hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, float alpha,
                             const void* q_train, const void* q_test, const void* k,
                             const void* v, void* o_train, void* o_test, hipStream_t s);
 

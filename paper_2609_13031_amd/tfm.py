@@ -33,7 +33,10 @@ SIGNATURES = {
     "tfm_icl_attention_fp8_prequantized_workspace_bytes": (_c_size, [_c_int] * 4),
     "tfm_icl_attention_fp8_prequantized": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 10 + [_c_size, _p]),
     "tfm_icl_attention_fp8_block_kv": (_c_int, [_c_int]),
-    "tfm_icl_attention_bf16": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 6 + [_p]),
+    "tfm_icl_attention_bf16": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 6 + [_p]),
+    "tfm_icl_attention_workspace_bytes": (_c_size, [_c_int] * 6),
+    "tfm_icl_attention": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 6 + [_c_int, ctypes.POINTER(_c_int), _p,
+                                                                          _c_size, _p]),
 }
 
 
@@ -162,6 +165,11 @@ def tfm_quantize_qkv_per_head(q_train, k, v, q_test=None):
 def _outputs(B, H, D, N, M, out_dtype, dev, out):
     if out is not None:
         o_tr, o_te = out
+        if o_te is None:
+            o_te = torch.empty((B, 0, H, D), dtype=out_dtype, device=dev)
+        for t, rows in ((o_tr, N), (o_te, M)):
+            if tuple(t.shape) != (B, rows, H, D) or t.dtype != out_dtype or not t.is_contiguous():
+                raise ValueError("output tensors must be contiguous (B, rows, H, D) of the output dtype")
     else:
         o_tr = torch.empty((B, N, H, D), dtype=out_dtype, device=dev)
         o_te = torch.empty((B, M, H, D), dtype=out_dtype, device=dev)
@@ -229,12 +237,34 @@ def tfm_icl_attention_fp8_prequantized(q8_train, k8, v8, q8_test, s_q, s_k, s_v,
 
 
 def tfm_icl_attention_bf16(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None):
-    """The bf16 baseline of both ICL calls; returns (o_train, o_test)."""
+    """The 16-bit baseline of both ICL calls (bf16, or fp32 rounded to bf16 on load); returns (o_train, o_test)."""
     B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
-    if out_dtype not in _DTYPES:
-        raise ValueError("outputs must be float32 or bfloat16")
-    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, torch.bfloat16)
+    if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
     o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
-    _call("tfm_icl_attention_bf16", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D), _ptr(q_train), _ptr(k),
-          _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
+    _call("tfm_icl_attention_bf16", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+          _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
     return o_tr, o_te
+
+
+FP8_MIN_TRAIN_ROWS_DEFAULT = 8192
+
+
+def tfm_icl_attention(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, fp8_min_train_rows=-1,
+                      out=None, workspace=None):
+    """Gated ICL attention: FP8 when N > fp8_min_train_rows (default 8192), else the 16-bit path.
+
+    Returns (o_train, o_test, used_fp8)."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    nws = lib().tfm_icl_attention_workspace_bytes(B, H, D, N, M, int(fp8_min_train_rows))
+    ws = workspace if workspace is not None else (torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None)
+    used = ctypes.c_int(-1)
+    _call("tfm_icl_attention", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+          _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None),
+          int(fp8_min_train_rows), ctypes.byref(used), _ptr(ws), 0 if ws is None else ws.numel(), _stream())
+    return o_tr, o_te, bool(used.value)

@@ -20,7 +20,7 @@ def header_functions():
 def test_library_exports_every_declared_function():
     L = tfm.lib()
     names = header_functions()
-    assert len(names) == 12
+    assert len(names) == 14
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(tfm.SIGNATURES)
@@ -50,7 +50,7 @@ def test_block_kv_and_workspace_queries():
     assert tfm.tfm_icl_attention_fp8_prequantized_workspace_bytes(1, 2, 128, 100) == 2 * 128 * 128
 
 
-FAKE = 0x10000          # aligned, never dereferenced: validation fails first
+FAKE = 0x10000          # aligned, never dereferenced: every call below fails validation first
 MIS = 0x10008           # 8-byte aligned only
 
 
@@ -89,9 +89,11 @@ def test_quantize_and_bf16_and_prequantized_validation():
                                                  FAKE, FAKE, FAKE, None, FAKE, FAKE, kw.get("v8", FAKE), None,
                                                  FAKE, FAKE, FAKE, FAKE, kw.get("nws", 1 << 20), None)
     assert q(dt=5) == 3 and q(B=0) == 2 and q(D=100) == 4 and q(v8=None) == 1 and q(v8=MIS) == 5 and q(nws=8) == 6
-    b = lambda **kw: L.tfm_icl_attention_bf16(kw.get("out", 1), 1, 2, 64, kw.get("N", 50), 3, kw.get("alpha", 0.1),
-                                              FAKE, FAKE, FAKE, kw.get("qt", FAKE), FAKE, FAKE, None)
-    assert b(out=3) == 3 and b(N=0) == 2 and b(alpha=-2.0) == 8 and b(qt=None) == 1 and b(qt=MIS) == 5
+    b = lambda **kw: L.tfm_icl_attention_bf16(kw.get("inp", 1), kw.get("out", 1), 1, 2, 64, kw.get("N", 50), 3,
+                                              kw.get("alpha", 0.1), FAKE, FAKE, FAKE, kw.get("qt", FAKE), FAKE, FAKE,
+                                              None)
+    assert b(out=3) == 3 and b(inp=4) == 3 and b(N=0) == 2 and b(alpha=-2.0) == 8 and b(qt=None) == 1
+    assert b(qt=MIS) == 5
     qs = lambda **kw: L.tfm_icl_attention_fp8_quantize(1, 1, 2, 64, 50, kw.get("M", 3), FAKE, FAKE, FAKE,
                                                        kw.get("qt", FAKE), FAKE, kw.get("nws", 1 << 30), None)
     assert qs(qt=None) == 1 and qs(M=0, qt=None, nws=10) == 6 and qs(qt=MIS) == 5
@@ -102,3 +104,21 @@ def test_quantize_and_bf16_and_prequantized_validation():
                                                           kw.get("sk", FAKE), FAKE, FAKE, None, FAKE,
                                                           kw.get("nws", 1 << 20), None)
     assert p(sk=None) == 1 and p(nws=100) == 6
+
+
+def test_gate_selects_the_path_before_validating_it():
+    L = tfm.lib()
+    used = ctypes.c_int(-7)
+    g = lambda N, gate, **kw: L.tfm_icl_attention(1, 1, 1, 2, 64, N, 3, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, gate,
+                                                  ctypes.byref(used), kw.get("ws", FAKE), kw.get("nws", 0), None)
+    # The FP8 path needs a workspace, the 16-bit path none: the reported error
+    # tells which one validated.  (Every call here must fail validation: the
+    # pointers are fake and must never reach a kernel.)
+    assert g(8193, -1) == 6 and g(9000, 8192) == 6 and g(100, 50) == 6
+    assert L.tfm_icl_attention(1, 1, 1, 2, 64, 8192, 3, 0.1, FAKE, FAKE, FAKE, None, FAKE, FAKE, -1,
+                               ctypes.byref(used), None, 0, None) == 1      # 16-bit path: NULL q_test with M > 0
+    assert used.value == -7                        # not written on failure
+    assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 8192, 3, -1) == 0
+    assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 8193, 3, -1) == tfm.tfm_icl_attention_fp8_workspace_bytes(
+        1, 2, 64, 8193, 3)
+    assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 100, 3, 99) > 0

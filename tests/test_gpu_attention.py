@@ -258,3 +258,30 @@ def test_bf16_kernel_invariances(thr):
     c = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha, out_dtype=torch.bfloat16)
     assert torch.equal(a[0], b[0])
     assert torch.equal(c[0], a[0].to(torch.bfloat16)) and torch.equal(c[1], a[1].to(torch.bfloat16))
+
+
+# ---------------- gate and 16-bit path with fp32 inputs ----------------
+
+@pytest.mark.parametrize("N,expect_fp8", [(8192, False), (8193, True)])
+def test_gate_runs_fp8_only_above_8192_train_rows(N, expect_fp8):
+    w = Workload("gate", B=1, H=1, D=64, N=N, M=16, dtype="bf16", seed=N)
+    g = gpu_inputs(generate(w), torch.bfloat16)
+    o_tr, o_te, used = tfm.tfm_icl_attention(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    assert used == expect_fp8
+    direct = (tfm.tfm_icl_attention_fp8 if expect_fp8 else tfm.tfm_icl_attention_bf16)(
+        g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    assert torch.equal(o_tr, direct[0]) and torch.equal(o_te, direct[1])
+    # an explicit gate moves the switch
+    _, _, used2 = tfm.tfm_icl_attention(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha,
+                                        fp8_min_train_rows=N - 1)
+    assert used2
+
+
+def test_bf16_kernel_rounds_fp32_inputs_to_bf16_on_load():
+    w = Workload("f32in", B=1, H=2, D=64, N=700, M=33, dtype="f32", seed=31)
+    x = generate(w)
+    g32 = gpu_inputs(x, torch.float32)
+    g16 = {k: v.to(torch.bfloat16) for k, v in g32.items()}
+    a = tfm.tfm_icl_attention_bf16(g32["q_train"], g32["k"], g32["v"], g32["q_test"], alpha=w.alpha)
+    b = tfm.tfm_icl_attention_bf16(g16["q_train"], g16["k"], g16["v"], g16["q_test"], alpha=w.alpha)
+    assert torch.equal(a[0], b[0]) and torch.equal(a[1], b[1])
