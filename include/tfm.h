@@ -54,10 +54,36 @@ typedef enum {
   TFM_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
   TFM_ERR_WORKSPACE_TOO_SMALL = 6,  /* workspace_bytes below the size query */
   TFM_ERR_HIP = 7,                  /* the HIP runtime reported an error */
-  TFM_ERR_BAD_ARG = 8               /* alpha is not finite and positive */
+  TFM_ERR_BAD_ARG = 8               /* alpha not finite and positive, or a bad option */
 } tfm_status;
 
 typedef enum { TFM_F32 = 0, TFM_BF16 = 1 } tfm_dtype;
+
+/*
+ * Options of the ICL calls (host memory; a NULL pointer means all defaults).
+ *
+ * q_scale_mode -- which dynamic scale the test queries are quantized with:
+ *   TFM_QSCALE_SHARED   (0, default) the per-head scale of the train queries,
+ *                       which makes test predictions independent of the test
+ *                       batch (Sec. 3, the paragraph after Eq. (2); Table 1,
+ *                       last row: the paper's final choice);
+ *   TFM_QSCALE_PER_CALL (1) their own per-head absmax scale, computed over the
+ *                       test rows of the call (Table 1, "per-call query scale");
+ *   TFM_QSCALE_JOINT    (2) one per-head scale over the train and test queries
+ *                       together, as for the single ICL call the paper uses for
+ *                       TabICLv2 (Appendix, "Experiments on TabICLv2").
+ * test_kv_heads -- the K/V heads the test rows attend to.  0 (default) or H:
+ *   query head h attends to K/V head h, as the train rows do.  1 <= G < H with
+ *   H % G == 0: grouped-query attention of the test rows over the first G K/V
+ *   heads (query head h uses K/V head h / (H / G)), the way TabPFN-v3's test
+ *   rows attend to the first K/V head (Appendix A).  The test call then reads
+ *   exactly the quantized K/V (codes and scales) the train call reads.
+ */
+typedef enum { TFM_QSCALE_SHARED = 0, TFM_QSCALE_PER_CALL = 1, TFM_QSCALE_JOINT = 2 } tfm_qscale_mode;
+typedef struct tfm_icl_options {
+  int q_scale_mode;
+  int test_kv_heads;
+} tfm_icl_options;
 
 /* A hipStream_t, passed as an opaque pointer. */
 typedef void* tfm_stream;
@@ -74,24 +100,27 @@ int tfm_version(void);
  * For every (b, h): s_q = fl32(max|Q_train| / 448), s_k and s_v likewise
  * (fp32 division; a head whose scale would be 0 gets scale 1), and each
  * element becomes the e4m3fn code of clamp(fl32(x / s), -448, 448), rounded
- * to nearest, ties to even.  Q_test is quantized with s_q of Q_train.
+ * to nearest, ties to even.  Q_test is quantized with s_q_test, which is s_q
+ * of Q_train unless opts->q_scale_mode says otherwise (see tfm_icl_options).
  *
  *   in_dtype            TFM_F32 or TFM_BF16, the element type of the inputs
+ *   opts                NULL or the options (only q_scale_mode is used)
  *   q_train, k, v       (B, N, H, D) inputs
  *   q_test              (B, M, H, D) input, NULL iff M == 0
  *   q8_train, k8, v8    (B, H, N, D) uint8 outputs
  *   q8_test             (B, H, M, D) uint8 output, NULL iff M == 0
  *   s_q, s_k, s_v       (B, H) float32 outputs
+ *   s_q_test            (B, H) float32 output: the scale of Q_test (may be NULL)
  *   workspace           >= tfm_quantize_workspace_bytes(B, H) device bytes
  *                       of scratch (contents on entry are ignored)
  */
 size_t tfm_quantize_workspace_bytes(int B, int H);
-int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M,
-                              const void* q_train, const void* k, const void* v,
+int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, int H, int D, int N,
+                              int M, const void* q_train, const void* k, const void* v,
                               const void* q_test, uint8_t* q8_train, uint8_t* k8,
                               uint8_t* v8, uint8_t* q8_test, float* s_q, float* s_k,
-                              float* s_v, void* workspace, size_t workspace_bytes,
-                              tfm_stream stream);
+                              float* s_v, float* s_q_test, void* workspace,
+                              size_t workspace_bytes, tfm_stream stream);
 
 /*
  * tfm_icl_attention_fp8 -- the full hot path: Eq. (2) quantization of
@@ -109,6 +138,10 @@ int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M,
  *
  *   in_dtype            TFM_F32 or TFM_BF16 (inputs)
  *   out_dtype           TFM_F32 or TFM_BF16 (outputs)
+ *   opts                NULL (defaults) or the options: query-scale mode and
+ *                       grouped test K/V heads (see tfm_icl_options); test rows
+ *                       use c = alpha * s_q_test * s_k(h') * log2(e) and s_v(h')
+ *                       of their K/V head h'
  *   alpha               softmax scale (finite, > 0), usually 1/sqrt(D)
  *   q_train, k, v       (B, N, H, D);  q_test (B, M, H, D), NULL iff M == 0
  *   o_train             (B, N, H, D) output;  o_test (B, M, H, D), NULL iff M == 0
@@ -117,8 +150,8 @@ int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M,
  *                       it holds the codes and scales of the call
  */
 size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M);
-int tfm_icl_attention_fp8(int in_dtype, int out_dtype, int B, int H, int D, int N, int M,
-                          float alpha, const void* q_train, const void* k, const void* v,
+int tfm_icl_attention_fp8(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H,
+                          int D, int N, int M, float alpha, const void* q_train, const void* k, const void* v,
                           const void* q_test, void* o_train, void* o_test, void* workspace,
                           size_t workspace_bytes, tfm_stream stream);
 
@@ -132,15 +165,18 @@ int tfm_icl_attention_fp8(int in_dtype, int out_dtype, int B, int H, int D, int 
  *   (on the train-query scale) into `workspace`, in the private layout the
  *   attention stage reads (arguments as for tfm_icl_attention_fp8).
  * tfm_icl_attention_fp8_attend -- both ICL calls from a workspace filled by
- *   tfm_icl_attention_fp8_quantize with the same B, H, D, N, M; the
- *   workspace is only read.  Outputs as for tfm_icl_attention_fp8.
+ *   tfm_icl_attention_fp8_quantize with the same B, H, D, N, M and query-
+ *   scale mode; the workspace is only read.  Outputs as for
+ *   tfm_icl_attention_fp8.
  */
-int tfm_icl_attention_fp8_quantize(int in_dtype, int B, int H, int D, int N, int M,
+int tfm_icl_attention_fp8_quantize(int in_dtype, const tfm_icl_options* opts, int B, int H, int D,
+                                   int N, int M,
                                    const void* q_train, const void* k, const void* v,
                                    const void* q_test, void* workspace, size_t workspace_bytes,
                                    tfm_stream stream);
-int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                                 void* o_train, void* o_test, const void* workspace,
+int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int B, int H, int D,
+                                 int N, int M, float alpha, void* o_train, void* o_test,
+                                 const void* workspace,
                                  size_t workspace_bytes, tfm_stream stream);
 
 /*
@@ -150,16 +186,18 @@ int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int 
  * several test batches.  The workspace receives a re-laid-out copy of V_8.
  *
  *   q8_train, k8, v8    (B, H, N, D) uint8;  q8_test (B, H, M, D), NULL iff M == 0
- *   s_q, s_k, s_v       (B, H) float32
+ *   s_q, s_k, s_v       (B, H) float32;  s_q_test (B, H) float32 or NULL (then s_q)
+ *   opts                NULL or the options (only test_kv_heads is used)
  *   workspace           >= tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
  */
 size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, int N);
-int tfm_icl_attention_fp8_prequantized(int out_dtype, int B, int H, int D, int N, int M,
-                                       float alpha, const uint8_t* q8_train,
-                                       const uint8_t* k8, const uint8_t* v8,
-                                       const uint8_t* q8_test, const float* s_q,
-                                       const float* s_k, const float* s_v, void* o_train,
-                                       void* o_test, void* workspace, size_t workspace_bytes,
+int tfm_icl_attention_fp8_prequantized(int out_dtype, const tfm_icl_options* opts, int B, int H,
+                                       int D, int N, int M, float alpha,
+                                       const uint8_t* q8_train, const uint8_t* k8,
+                                       const uint8_t* v8, const uint8_t* q8_test,
+                                       const float* s_q, const float* s_k, const float* s_v,
+                                       const float* s_q_test, void* o_train, void* o_test,
+                                       void* workspace, size_t workspace_bytes,
                                        tfm_stream stream);
 
 /* Number of keys per tile of the FP8 kernel for head_dim D (the granularity
@@ -173,12 +211,13 @@ int tfm_icl_attention_fp8_block_kv(int D);
  * product and normalised by the sum of the rounded P, fp32 accumulation.
  *
  *   in_dtype            TFM_BF16 or TFM_F32
+ *   opts                NULL or the options (only test_kv_heads is used)
  *   q_train, k, v       (B, N, H, D);  q_test (B, M, H, D), NULL iff M == 0
  *   out_dtype           TFM_F32 or TFM_BF16
  *   o_train, o_test     as for tfm_icl_attention_fp8
  */
-int tfm_icl_attention_bf16(int in_dtype, int out_dtype, int B, int H, int D, int N, int M,
-                           float alpha, const void* q_train, const void* k, const void* v,
+int tfm_icl_attention_bf16(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H,
+                           int D, int N, int M, float alpha, const void* q_train, const void* k, const void* v,
                            const void* q_test, void* o_train, void* o_test, tfm_stream stream);
 
 /*
@@ -193,7 +232,8 @@ int tfm_icl_attention_bf16(int in_dtype, int out_dtype, int B, int H, int D, int
  */
 #define TFM_FP8_MIN_TRAIN_ROWS_DEFAULT 8192
 size_t tfm_icl_attention_workspace_bytes(int B, int H, int D, int N, int M, int fp8_min_train_rows);
-int tfm_icl_attention(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
+int tfm_icl_attention(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D,
+                      int N, int M, float alpha,
                       const void* q_train, const void* k, const void* v, const void* q_test,
                       void* o_train, void* o_test, int fp8_min_train_rows, int* used_fp8,
                       void* workspace, size_t workspace_bytes, tfm_stream stream);

@@ -6,7 +6,11 @@
 * ``icl_attention`` -- the ICL stage evaluates Eq. (1) twice per head: the N
   train queries and the M test queries both attend to the same N train keys
   and values (Sec. 3, second paragraph).  Used on the exact inputs (O_exact)
-  and on the dequantized inputs s*X_8 (O_q).
+  and on the dequantized inputs s*X_8 (O_q).  With ``test_kv_heads`` G < H
+  the test call is grouped-query attention over the first G heads of the
+  train K/V: query head h reads K/V head h // (H / G).  TabPFN-v3's test
+  rows attend to the first K/V head this way (G = 1), and the two calls then
+  consume the very same K/V entries (appendix, noise experiment).
 * ``icl_attention_fp8_kernel_model`` -- a replay, in fp64, of the one-pass
   fused kernel the paper describes (Sec. 3 and Fig. 2): tiles of ``block_kv``
   keys in order, a running row maximum, the Q and K scales applied together
@@ -51,7 +55,15 @@ def _pick(rows, n):
     return np.arange(n) if rows is None else np.asarray(rows, dtype=np.int64)
 
 
-def icl_attention(q_train, k, v, q_test, alpha, rows_train=None, rows_test=None):
+def grouped_kv_head(h, H, test_kv_heads):
+    """The K/V head that test query head h reads (test_kv_heads None or 0 means H)."""
+    G = H if not test_kv_heads else int(test_kv_heads)
+    if G < 1 or G > H or H % G:
+        raise ValueError("test_kv_heads must divide H")
+    return h // (H // G)
+
+
+def icl_attention(q_train, k, v, q_test, alpha, rows_train=None, rows_test=None, test_kv_heads=None):
     """Train-train and test-train attention on (B,S,H,D) inputs, fp64.
 
     Returns (o_train, o_test) with shapes (B, R_train, H, D) and
@@ -70,7 +82,8 @@ def icl_attention(q_train, k, v, q_test, alpha, rows_train=None, rows_test=None)
             vv = v[b, :, h, :]
             o_tr[b, :, h] = softmax_attention(q_train[b, rt, h, :], kk, vv, alpha)
             if len(re):
-                o_te[b, :, h] = softmax_attention(q_test[b, re, h, :], kk, vv, alpha)
+                hk = grouped_kv_head(h, H, test_kv_heads)
+                o_te[b, :, h] = softmax_attention(q_test[b, re, h, :], k[b, :, hk, :], v[b, :, hk, :], alpha)
     return o_tr, o_te
 
 
@@ -80,13 +93,14 @@ def dequantize(codes, scale):
     return x.transpose(0, 2, 1, 3)
 
 
-def icl_attention_dequantized(qz, alpha, rows_train=None, rows_test=None):
-    """O_q: Eq. (1) in fp64 on the dequantized tensors of ``quantize_qkv_per_head``."""
-    q_te = dequantize(qz["q8_test"], qz["s_q"]) if "q8_test" in qz else None
+def icl_attention_dequantized(qz, alpha, rows_train=None, rows_test=None, test_kv_heads=None):
+    """O_q: Eq. (1) in fp64 on the dequantized tensors of ``quantize_qkv_per_head``
+    (test queries with their own scale s_q_test)."""
+    q_te = dequantize(qz["q8_test"], qz.get("s_q_test", qz["s_q"])) if "q8_test" in qz else None
     return icl_attention(dequantize(qz["q8_train"], qz["s_q"]),
                          dequantize(qz["k8"], qz["s_k"]),
                          dequantize(qz["v8"], qz["s_v"]),
-                         q_te, alpha, rows_train, rows_test)
+                         q_te, alpha, rows_train, rows_test, test_kv_heads)
 
 
 def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_sum="p8", tie_rel=None):
@@ -130,12 +144,14 @@ def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_su
 
 
 def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_test=None,
-                                   quantize_p=True, row_sum="p8", tie_rel=None):
+                                   quantize_p=True, row_sum="p8", tie_rel=None, test_kv_heads=None):
     """O_qp: both ICL calls through ``one_pass_fp8_attention`` for every (b, h).
 
-    ``qz`` is the output of ``quantize_qkv_per_head``.  Returns (o_train,
-    o_test) as (B, R, H, D) fp64 for the selected rows; with ``tie_rel`` set,
-    returns ((o_train, allowance_train), (o_test, allowance_test)).
+    ``qz`` is the output of ``quantize_qkv_per_head``.  The test call of head
+    h uses the test-query scale s_q_test and the codes and scales of K/V head
+    ``grouped_kv_head(h, H, test_kv_heads)``.  Returns (o_train, o_test) as
+    (B, R, H, D) fp64 for the selected rows; with ``tie_rel`` set, returns
+    ((o_train, allowance_train), (o_test, allowance_test)).
     """
     B, H, N, D = qz["k8"].shape
     rt = _pick(rows_train, N)
@@ -145,15 +161,18 @@ def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_te
     o_te = np.zeros((B, len(re), H, D))
     a_tr = np.zeros_like(o_tr)
     a_te = np.zeros_like(o_te)
+    s_q_test = qz.get("s_q_test", qz["s_q"])
     for b in range(B):
         for h in range(H):
-            c = float(alpha) * float(qz["s_q"][b, h]) * float(qz["s_k"][b, h]) * LOG2E
-            kq = decode(qz["k8"][b, h])
-            vq = decode(qz["v8"][b, h])
-            args = (kq, vq, c, qz["s_v"][b, h], block_kv, quantize_p, row_sum, tie_rel)
-            for o, a, key, rows in ((o_tr, a_tr, "q8_train", rt), (o_te, a_te, "q8_test", re)):
+            hk = grouped_kv_head(h, H, test_kv_heads)
+            calls = ((o_tr, a_tr, "q8_train", rt, qz["s_q"][b, h], h),
+                     (o_te, a_te, "q8_test", re, s_q_test[b, h], hk))
+            for o, a, key, rows, s_query, hkv in calls:
                 if len(rows) == 0:
                     continue
+                c = float(alpha) * float(s_query) * float(qz["s_k"][b, hkv]) * LOG2E
+                args = (decode(qz["k8"][b, hkv]), decode(qz["v8"][b, hkv]), c, qz["s_v"][b, hkv], block_kv,
+                        quantize_p, row_sum, tie_rel)
                 res = one_pass_fp8_attention(decode(qz[key][b, h, rows]), *args)
                 if tie_rel is None:
                     o[b, :, h] = res

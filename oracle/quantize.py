@@ -8,7 +8,11 @@ computed from the tensor itself (no calibration).  In the ICL layer keys and
 values come from the train rows only, and the test queries are quantized
 with the scale of the *train* queries, which makes test predictions
 independent of the test batch (Sec. 3, paragraph after Eq. (2); Table 1,
-last row).
+last row).  Two other query-scale choices the paper evaluates are modes of
+``quantize_qkv_per_head``: "per_call" gives the test queries their own
+per-head scale (Table 1, "both, per-call query scale"), and "joint" takes one
+per-head scale over train and test queries together, as a single attention
+call over all rows does (the appendix's TabICLv2 experiments).
 
 Readings where the paper is silent (each also listed in the design notes):
 * granularity: one scale per (table b, head h), over all rows and channels;
@@ -55,23 +59,42 @@ def quantize_with_scale(x, s):
     return np.ascontiguousarray(codes.transpose(0, 2, 1, 3))
 
 
-def quantize_qkv_per_head(q_train, k, v, q_test=None):
+Q_SCALE_MODES = ("shared", "per_call", "joint")
+
+
+def quantize_qkv_per_head(q_train, k, v, q_test=None, q_scale_mode="shared"):
     """Eq. (2) applied to the ICL layer's tensors.
 
-    Q_train, K and V get their own per-head scales; Q_test (optional) is
-    quantized with the scale of Q_train.  Returns a dict with the codes
+    K and V get their own per-head scales.  The queries' scales follow
+    ``q_scale_mode``:
+      "shared"   -- s_q from Q_train; Q_test is quantized with s_q as well;
+      "per_call" -- s_q from Q_train, s_q_test from Q_test alone;
+      "joint"    -- one scale s_q = s_q_test from the absmax over Q_train and
+                    Q_test together.
+    A missing or empty Q_test has absmax 0.  Returns a dict with the codes
     ``q8_train, k8, v8, q8_test`` ((B,H,S,D) uint8) and the scales
-    ``s_q, s_k, s_v`` ((B,H) float32).
+    ``s_q, s_k, s_v, s_q_test`` ((B,H) float32).
     """
-    s_q = scale_from_amax(absmax_per_head(q_train))
+    if q_scale_mode not in Q_SCALE_MODES:
+        raise ValueError("q_scale_mode must be one of %s" % (Q_SCALE_MODES,))
+    a_q = absmax_per_head(q_train)
+    if q_test is None:
+        a_qt = np.zeros_like(a_q)
+    else:
+        a_qt = absmax_per_head(q_test)
+    if q_scale_mode == "joint":
+        s_q = scale_from_amax(np.maximum(a_q, a_qt))
+    else:
+        s_q = scale_from_amax(a_q)
+    s_q_test = scale_from_amax(a_qt) if q_scale_mode == "per_call" else s_q
     s_k = scale_from_amax(absmax_per_head(k))
     s_v = scale_from_amax(absmax_per_head(v))
     out = {
         "q8_train": quantize_with_scale(q_train, s_q),
         "k8": quantize_with_scale(k, s_k),
         "v8": quantize_with_scale(v, s_v),
-        "s_q": s_q, "s_k": s_k, "s_v": s_v,
+        "s_q": s_q, "s_k": s_k, "s_v": s_v, "s_q_test": s_q_test,
     }
     if q_test is not None:
-        out["q8_test"] = quantize_with_scale(q_test, s_q)
+        out["q8_test"] = quantize_with_scale(q_test, s_q_test)
     return out

@@ -18,8 +18,8 @@ Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M) {
   Fp8Workspace w;
   const size_t bh = (size_t)B * H;
   size_t off = 0;
-  w.amax = off;      off += align256(3 * bh * sizeof(uint32_t));
-  w.scales = off;    off += align256(3 * bh * sizeof(float));
+  w.amax = off;      off += align256(4 * bh * sizeof(uint32_t));
+  w.scales = off;    off += align256(4 * bh * sizeof(float));
   w.q8_train = off;  off += align256(bh * N * D);
   w.q8_test = off;   off += align256(bh * (size_t)M * D);
   w.k8 = off;        off += align256(bh * N * D);
@@ -44,7 +44,8 @@ int check_shape(int B, int H, int D, int N, int M) {
   if ((long long)B * H > 65535) return TFM_ERR_BAD_SHAPE;
   if ((long long)N + M > (long long)INT_MAX - 256) return TFM_ERR_BAD_SHAPE;
   if (D != 64 && D != 128) return TFM_ERR_UNSUPPORTED_HEAD_DIM;
-  if (((long long)N + M + 127) / 128 * B * H > (long long)INT_MAX) return TFM_ERR_BAD_SHAPE;  // attention grid
+  if (((long long)N + 127) / 128 + ((long long)M + 127) / 128 > (long long)INT_MAX / ((long long)B * H))
+    return TFM_ERR_BAD_SHAPE;  // attention grid: query tiles of the train rows, then of the test rows
   const long double elems = (long double)B * H * D * ((long double)N + M);
   if (elems > 281474976710656.0L) return TFM_ERR_BAD_SHAPE;
   return TFM_OK;
@@ -60,23 +61,44 @@ int check_io(bool need_test, const void* const* req, int nreq, const void* const
 
 int check_alpha(float alpha) { return (std::isfinite(alpha) && alpha > 0.0f) ? TFM_OK : TFM_ERR_BAD_ARG; }
 
+// Options with defaults filled in; TFM_ERR_BAD_ARG for an unknown query-scale
+// mode or a test K/V head count that is not 0 or a divisor of H.
+struct Opts {
+  int q_scale_mode = TFM_QSCALE_SHARED;
+  int test_kv_heads = 0;
+};
+int parse_opts(const tfm_icl_options* o, int H, Opts* out) {
+  Opts r;
+  if (o) {
+    r.q_scale_mode = o->q_scale_mode;
+    r.test_kv_heads = o->test_kv_heads;
+  }
+  if (r.q_scale_mode < TFM_QSCALE_SHARED || r.q_scale_mode > TFM_QSCALE_JOINT) return TFM_ERR_BAD_ARG;
+  if (r.test_kv_heads == 0) r.test_kv_heads = H;
+  if (r.test_kv_heads < 1 || r.test_kv_heads > H || H % r.test_kv_heads != 0) return TFM_ERR_BAD_ARG;
+  *out = r;
+  return TFM_OK;
+}
+
 int hip_status(hipError_t e) { return e == hipSuccess ? TFM_OK : TFM_ERR_HIP; }
 
 #define TFM_TRY(expr) do { int st_ = (expr); if (st_ != TFM_OK) return st_; } while (0)
 #define TFM_HIP(expr) do { if ((expr) != hipSuccess) return TFM_ERR_HIP; } while (0)
 
 // amax + scales + the four code tensors.  v8 == nullptr writes V to v8t instead.
-int quantize_all(int in_dtype, int B, int H, int D, int N, int M, const void* q_train, const void* k,
-                 const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8, uint8_t* v8t,
-                 uint8_t* q8_test, uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
-                 hipStream_t s) {
+// amax holds 4*B*H words and scales 4*B*H floats (s_q, s_k, s_v, s_q_test).
+int quantize_all(int in_dtype, int q_scale_mode, int B, int H, int D, int N, int M, const void* q_train,
+                 const void* k, const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8,
+                 uint8_t* v8t, uint8_t* q8_test, uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
+                 float* s_q_test, hipStream_t s) {
   const int bf = in_dtype == TFM_BF16;
   const int BH = B * H;
-  TFM_HIP(launch_fill_zero_u32(amax, 3 * BH, s));
-  TFM_HIP(launch_amax(bf, B, H, D, N, q_train, k, v, amax, s));
-  TFM_HIP(launch_scales(BH, amax, scales, s_q, s_k, s_v, s));
+  const bool test_amax = q_scale_mode != TFM_QSCALE_SHARED && M > 0;
+  TFM_HIP(launch_fill_zero_u32(amax, 4 * BH, s));
+  TFM_HIP(launch_amax(bf, B, H, D, N, M, q_train, k, v, test_amax ? q_test : nullptr, amax, s));
+  TFM_HIP(launch_scales(BH, q_scale_mode, amax, scales, s_q, s_k, s_v, s_q_test, s));
   TFM_HIP(launch_quantize_rows(bf, B, H, D, N, q_train, scales, q8_train, s));
-  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales, q8_test, s));
+  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, q8_test, s));
   TFM_HIP(launch_quantize_rows(bf, B, H, D, N, k, scales + BH, k8, s));
   if (v8) TFM_HIP(launch_quantize_rows(bf, B, H, D, N, v, scales + 2 * BH, v8, s));
   else TFM_HIP(launch_quantize_v_tiles(bf, B, H, D, N, v, scales + 2 * BH, v8t, s));
@@ -97,33 +119,39 @@ const char* tfm_status_string(int status) {
     case TFM_ERR_MISALIGNED: return "TFM_ERR_MISALIGNED: pointers must be 16-byte aligned";
     case TFM_ERR_WORKSPACE_TOO_SMALL: return "TFM_ERR_WORKSPACE_TOO_SMALL: workspace below the size query";
     case TFM_ERR_HIP: return "TFM_ERR_HIP: the HIP runtime reported an error";
-    case TFM_ERR_BAD_ARG: return "TFM_ERR_BAD_ARG: alpha must be finite and positive";
+    case TFM_ERR_BAD_ARG:
+      return "TFM_ERR_BAD_ARG: alpha must be finite and positive, q_scale_mode one of TFM_QSCALE_*, "
+             "test_kv_heads 0 or a divisor of H";
     default: return "TFM_ERR_UNKNOWN";
   }
 }
 
-int tfm_version(void) { return 100; }
+int tfm_version(void) { return 200; }
 
 size_t tfm_quantize_workspace_bytes(int B, int H) {
   if (B < 1 || H < 1) return 0;
-  return align256(3 * (size_t)B * H * sizeof(uint32_t)) + align256(3 * (size_t)B * H * sizeof(float));
+  return align256(4 * (size_t)B * H * sizeof(uint32_t)) + align256(4 * (size_t)B * H * sizeof(float));
 }
 
-int tfm_quantize_qkv_per_head(int in_dtype, int B, int H, int D, int N, int M, const void* q_train, const void* k,
-                              const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8,
-                              uint8_t* q8_test, float* s_q, float* s_k, float* s_v, void* workspace,
-                              size_t workspace_bytes, tfm_stream stream) {
+int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
+                              const void* q_train, const void* k, const void* v, const void* q_test,
+                              uint8_t* q8_train, uint8_t* k8, uint8_t* v8, uint8_t* q8_test, float* s_q, float* s_k,
+                              float* s_v, float* s_q_test, void* workspace, size_t workspace_bytes,
+                              tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {q_train, k, v, q8_train, k8, v8, s_q, s_k, s_v, workspace};
   const void* tst[] = {q_test, q8_test};
   TFM_TRY(check_io(M > 0, req, 10, tst, 2));
+  if (s_q_test && !aligned16(s_q_test)) return TFM_ERR_MISALIGNED;
   if (workspace_bytes < tfm_quantize_workspace_bytes(B, H)) return TFM_ERR_WORKSPACE_TOO_SMALL;
   uint8_t* ws = (uint8_t*)workspace;
   uint32_t* amax = (uint32_t*)ws;
-  float* scales = (float*)(ws + align256(3 * (size_t)B * H * sizeof(uint32_t)));
-  return quantize_all(in_dtype, B, H, D, N, M, q_train, k, v, q_test, q8_train, k8, v8, nullptr, q8_test, amax,
-                      scales, s_q, s_k, s_v, (hipStream_t)stream);
+  float* scales = (float*)(ws + align256(4 * (size_t)B * H * sizeof(uint32_t)));
+  return quantize_all(in_dtype, o.q_scale_mode, B, H, D, N, M, q_train, k, v, q_test, q8_train, k8, v8, nullptr,
+                      q8_test, amax, scales, s_q, s_k, s_v, s_q_test, (hipStream_t)stream);
 }
 
 size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M) {
@@ -131,27 +159,32 @@ size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M) 
   return fp8_workspace_layout(B, H, D, N, M).total;
 }
 
-int tfm_icl_attention_fp8_quantize(int in_dtype, int B, int H, int D, int N, int M, const void* q_train,
-                                   const void* k, const void* v, const void* q_test, void* workspace,
-                                   size_t workspace_bytes, tfm_stream stream) {
+int tfm_icl_attention_fp8_quantize(int in_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
+                                   const void* q_train, const void* k, const void* v, const void* q_test,
+                                   void* workspace, size_t workspace_bytes, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {q_train, k, v, workspace};
   const void* tst[] = {q_test};
   TFM_TRY(check_io(M > 0, req, 4, tst, 1));
   const Fp8Workspace L = fp8_workspace_layout(B, H, D, N, M);
   if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
   uint8_t* ws = (uint8_t*)workspace;
-  return quantize_all(in_dtype, B, H, D, N, M, q_train, k, v, q_test, ws + L.q8_train, ws + L.k8, nullptr,
-                      ws + L.v8t, ws + L.q8_test, (uint32_t*)(ws + L.amax), (float*)(ws + L.scales), nullptr,
-                      nullptr, nullptr, (hipStream_t)stream);
+  return quantize_all(in_dtype, o.q_scale_mode, B, H, D, N, M, q_train, k, v, q_test, ws + L.q8_train, ws + L.k8,
+                      nullptr, ws + L.v8t, ws + L.q8_test, (uint32_t*)(ws + L.amax), (float*)(ws + L.scales),
+                      nullptr, nullptr, nullptr, nullptr, (hipStream_t)stream);
 }
 
-int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int M, float alpha, void* o_train,
-                                 void* o_test, const void* workspace, size_t workspace_bytes, tfm_stream stream) {
+int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
+                                 float alpha, void* o_train, void* o_test, const void* workspace,
+                                 size_t workspace_bytes, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {o_train, workspace};
   const void* tst[] = {o_test};
   TFM_TRY(check_io(M > 0, req, 2, tst, 1));
@@ -160,26 +193,28 @@ int tfm_icl_attention_fp8_attend(int out_dtype, int B, int H, int D, int N, int 
   const uint8_t* ws = (const uint8_t*)workspace;
   const float* scales = (const float*)(ws + L.scales);
   const int BH = B * H;
-  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, alpha, ws + L.q8_train, ws + L.q8_test,
-                                    ws + L.k8, ws + L.v8t, scales, scales + BH, scales + 2 * BH, o_train, o_test,
-                                    (hipStream_t)stream));
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, o.test_kv_heads, alpha, ws + L.q8_train,
+                                    ws + L.q8_test, ws + L.k8, ws + L.v8t, scales, scales + BH, scales + 2 * BH,
+                                    scales + 3 * BH, o_train, o_test, (hipStream_t)stream));
 }
 
-int tfm_icl_attention_fp8(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                          const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
-                          void* o_test, void* workspace, size_t workspace_bytes, tfm_stream stream) {
+int tfm_icl_attention_fp8(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N,
+                          int M, float alpha, const void* q_train, const void* k, const void* v, const void* q_test,
+                          void* o_train, void* o_test, void* workspace, size_t workspace_bytes, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {q_train, k, v, o_train, workspace};
   const void* tst[] = {q_test, o_test};
   TFM_TRY(check_io(M > 0, req, 5, tst, 2));
   if (workspace_bytes < fp8_workspace_layout(B, H, D, N, M).total) return TFM_ERR_WORKSPACE_TOO_SMALL;
-  TFM_TRY(tfm_icl_attention_fp8_quantize(in_dtype, B, H, D, N, M, q_train, k, v, q_test, workspace, workspace_bytes,
-                                         stream));
-  return tfm_icl_attention_fp8_attend(out_dtype, B, H, D, N, M, alpha, o_train, o_test, workspace, workspace_bytes,
-                                      stream);
+  TFM_TRY(tfm_icl_attention_fp8_quantize(in_dtype, opts, B, H, D, N, M, q_train, k, v, q_test, workspace,
+                                         workspace_bytes, stream));
+  return tfm_icl_attention_fp8_attend(out_dtype, opts, B, H, D, N, M, alpha, o_train, o_test, workspace,
+                                      workspace_bytes, stream);
 }
 
 size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, int N) {
@@ -187,40 +222,45 @@ size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, i
   return align256(v8t_bytes(B, H, D, N));
 }
 
-int tfm_icl_attention_fp8_prequantized(int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                                       const uint8_t* q8_train, const uint8_t* k8, const uint8_t* v8,
-                                       const uint8_t* q8_test, const float* s_q, const float* s_k,
-                                       const float* s_v, void* o_train, void* o_test, void* workspace,
+int tfm_icl_attention_fp8_prequantized(int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
+                                       float alpha, const uint8_t* q8_train, const uint8_t* k8, const uint8_t* v8,
+                                       const uint8_t* q8_test, const float* s_q, const float* s_k, const float* s_v,
+                                       const float* s_q_test, void* o_train, void* o_test, void* workspace,
                                        size_t workspace_bytes, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {q8_train, k8, v8, s_q, s_k, s_v, o_train, workspace};
   const void* tst[] = {q8_test, o_test};
   TFM_TRY(check_io(M > 0, req, 8, tst, 2));
+  if (s_q_test && !aligned16(s_q_test)) return TFM_ERR_MISALIGNED;
   if (workspace_bytes < tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N))
     return TFM_ERR_WORKSPACE_TOO_SMALL;
   hipStream_t s = (hipStream_t)stream;
   uint8_t* v8t = (uint8_t*)workspace;
   TFM_HIP(launch_relayout_v_tiles(B, H, D, N, v8, v8t, s));
-  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, alpha, q8_train, q8_test, k8, v8t,
-                                    s_q, s_k, s_v, o_train, o_test, s));
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, o.test_kv_heads, alpha, q8_train, q8_test,
+                                    k8, v8t, s_q, s_k, s_v, s_q_test ? s_q_test : s_q, o_train, o_test, s));
 }
 
 int tfm_icl_attention_fp8_block_kv(int D) { return (D == 64 || D == 128) ? kBlockKv : 0; }
 
-int tfm_icl_attention_bf16(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                           const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
-                           void* o_test, tfm_stream stream) {
+int tfm_icl_attention_bf16(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N,
+                           int M, float alpha, const void* q_train, const void* k, const void* v, const void* q_test,
+                           void* o_train, void* o_test, tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
   TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
   const void* req[] = {q_train, k, v, o_train};
   const void* tst[] = {q_test, o_test};
   TFM_TRY(check_io(M > 0, req, 4, tst, 2));
-  return hip_status(launch_attn_bf16(in_dtype == TFM_F32, out_dtype == TFM_BF16, B, H, D, N, M, alpha, q_train,
-                                     q_test, k, v, o_train, o_test, (hipStream_t)stream));
+  return hip_status(launch_attn_bf16(in_dtype == TFM_F32, out_dtype == TFM_BF16, B, H, D, N, M, o.test_kv_heads, alpha,
+                                     q_train, q_test, k, v, o_train, o_test, (hipStream_t)stream));
 }
 
 static int gate_rows(int fp8_min_train_rows) {
@@ -232,19 +272,19 @@ size_t tfm_icl_attention_workspace_bytes(int B, int H, int D, int N, int M, int 
   return N > gate_rows(fp8_min_train_rows) ? fp8_workspace_layout(B, H, D, N, M).total : 0;
 }
 
-int tfm_icl_attention(int in_dtype, int out_dtype, int B, int H, int D, int N, int M, float alpha,
-                      const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
+int tfm_icl_attention(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
+                      float alpha, const void* q_train, const void* k, const void* v, const void* q_test, void* o_train,
                       void* o_test, int fp8_min_train_rows, int* used_fp8, void* workspace, size_t workspace_bytes,
                       tfm_stream stream) {
   TFM_TRY(check_shape(B, H, D, N, M));
   const bool fp8 = N > gate_rows(fp8_min_train_rows);
   int st;
   if (fp8)
-    st = tfm_icl_attention_fp8(in_dtype, out_dtype, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train, o_test,
-                               workspace, workspace_bytes, stream);
+    st = tfm_icl_attention_fp8(in_dtype, out_dtype, opts, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train,
+                               o_test, workspace, workspace_bytes, stream);
   else
-    st = tfm_icl_attention_bf16(in_dtype, out_dtype, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train, o_test,
-                                stream);
+    st = tfm_icl_attention_bf16(in_dtype, out_dtype, opts, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train,
+                                o_test, stream);
   if (st == TFM_OK && used_fp8) *used_fp8 = fp8 ? 1 : 0;
   return st;
 }

@@ -3,7 +3,8 @@
 // The same two ICL calls as the FP8 kernel (N train + M test query rows of
 // each (b, h) against the same N train keys/values, Eq. (1) of the paper)
 // with the same structure, without quantization:
-//  * a workgroup of 4 wave64s owns 128 query rows of one (b, h); 32 per wave;
+//  * a workgroup of 4 wave64s owns 128 train rows or 128 test rows of one
+//    (b, h); 32 per wave; test rows may attend to a shared K/V head;
 //  * key blocks of kBlockKvBf16 keys; K and V are staged through LDS in their
 //    row-major bf16 layout (double-buffered, one barrier per block);
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds the scores
@@ -31,7 +32,9 @@ typedef short v4s __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s lds_v4s;
 
 struct Bf16Args {
-  int B, H, N, M, tiles;
+  int B, H, N, M;
+  int tiles_train, tiles;  // query tiles per (b, h): train rows first, then test rows
+  int test_group;          // test rows of query head h read K/V head h / test_group
   float alpha;
   const void* q_train;
   const void* q_test;
@@ -126,14 +129,16 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   const int N = a.N, M = a.M;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int ql = lane % 32, half = lane / 32;
-  const int row = tile * kRowsPerBlock + wave * 32 + ql;
+  const bool test = tile >= a.tiles_train;
+  const int rows = test ? M : N;
+  const int row = (test ? tile - a.tiles_train : tile) * kRowsPerBlock + wave * 32 + ql;
+  const int hkv = test ? h / a.test_group : h;   // the K/V head the rows attend to
 
   // Q fragment: for head_dim chunk j (16 wide) the lane holds d in [16j + 8*half, +8)
   v8bf qf[D / 16];
   {
-    const T* qrow = nullptr;
-    if (row < N) qrow = (const T*)a.q_train + (((size_t)b * N + row) * H + h) * D;
-    else if (row < N + M) qrow = (const T*)a.q_test + (((size_t)b * M + (row - N)) * H + h) * D;
+    const T* qrow = row < rows ? (const T*)(test ? a.q_test : a.q_train) + (((size_t)b * rows + row) * H + h) * D
+                               : nullptr;
 #pragma unroll
     for (int j = 0; j < D / 16; ++j)
       qf[j] = qrow ? as_bf(load8_as_bf16(qrow + 16 * j + 8 * half)) : as_bf(u32x4{0u, 0u, 0u, 0u});
@@ -156,8 +161,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   v4f lacc = v4f{0.f, 0.f, 0.f, 0.f};
   float m_run = -__builtin_inff();
 
-  const T* kb_ptr = (const T*)a.k + ((size_t)b * N * H + h) * D;
-  const T* vb_ptr = (const T*)a.v + ((size_t)b * N * H + h) * D;
+  const T* kb_ptr = (const T*)a.k + ((size_t)b * N * H + hkv) * D;
+  const T* vb_ptr = (const T*)a.v + ((size_t)b * N * H + hkv) * D;
   const int row_stride = H * D;
   const int nblocks = (N + BKV - 1) / BKV;
 
@@ -243,9 +248,9 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
     __syncthreads();
   }
 
-  if (row >= N + M) return;
+  if (row >= rows) return;
   const float inv = 1.0f / lacc[0];
-  const size_t orow = row < N ? (((size_t)b * N + row) * H + h) * D : (((size_t)b * M + (row - N)) * H + h) * D;
+  const size_t orow = (((size_t)b * rows + row) * H + h) * D;
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) {
 #pragma unroll
@@ -254,11 +259,11 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
       const float o0 = acc_o[i][4 * g + 0] * inv, o1 = acc_o[i][4 * g + 1] * inv;
       const float o2 = acc_o[i][4 * g + 2] * inv, o3 = acc_o[i][4 * g + 3] * inv;
       if constexpr (OUT_BF16) {
-        __bf16* op = (row < N ? (__bf16*)a.o_train : (__bf16*)a.o_test) + orow + d;
+        __bf16* op = (test ? (__bf16*)a.o_test : (__bf16*)a.o_train) + orow + d;
         typedef __bf16 v4bf __attribute__((ext_vector_type(4)));
         *reinterpret_cast<v4bf*>(op) = v4bf{(__bf16)o0, (__bf16)o1, (__bf16)o2, (__bf16)o3};
       } else {
-        float* op = (row < N ? (float*)a.o_train : (float*)a.o_test) + orow + d;
+        float* op = (test ? (float*)a.o_test : (float*)a.o_train) + orow + d;
         *reinterpret_cast<v4f*>(op) = v4f{o0, o1, o2, o3};
       }
     }
@@ -279,12 +284,14 @@ static void launch_bf16_typed(int out_bf16, int D, const Bf16Args& a, dim3 grid,
   }
 }
 
-hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, float alpha,
-                            const void* q_train, const void* q_test, const void* k, const void* v, void* o_train,
-                            void* o_test, hipStream_t s) {
+hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads,
+                            float alpha, const void* q_train, const void* q_test, const void* k, const void* v,
+                            void* o_train, void* o_test, hipStream_t s) {
   Bf16Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
-  a.tiles = (N + M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.tiles_train = (N + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.tiles = a.tiles_train + (M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.test_group = H / test_kv_heads;
   a.alpha = alpha;
   a.q_train = q_train; a.q_test = q_test; a.k = k; a.v = v;
   a.o_train = o_train; a.o_test = o_test;

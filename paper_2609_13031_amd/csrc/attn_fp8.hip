@@ -1,9 +1,10 @@
 // Fused FP8 ICL attention on gfx950 (train-train and test-train in one launch).
 //
 // The kernel of Sec. 3 / Fig. 2 of the paper, laid out for CDNA4:
-//  * a workgroup of 4 wave64s owns 128 consecutive query rows of one (b, h)
-//    out of the N train + M test rows (both ICL calls share K_8 and V_8, so
-//    they are one launch); each wave owns 32 rows;
+//  * a workgroup of 4 wave64s owns 128 consecutive train rows or 128
+//    consecutive test rows of one (b, h) (both ICL calls share K_8 and V_8,
+//    so they are one launch); each wave owns 32 rows; test rows may attend to
+//    a shared K/V head (grouped-query test-train call);
 //  * key tiles of 64 are staged through LDS; per tile each wave computes
 //    S^T = K_8 Q_8^T with two v_mfma_f32_32x32x64_f8f6f4 per 64 of head_dim
 //    (fp32 accumulation), so every lane holds 32 scores of one query row;
@@ -29,7 +30,9 @@ constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
 constexpr int kPad = 16;  // LDS row padding (bytes): conflict-free 16-byte lane reads
 
 struct Fp8Args {
-  int B, H, N, M, tiles;
+  int B, H, N, M;
+  int tiles_train, tiles;  // query tiles per (b, h): train rows first, then test rows
+  int test_group;          // test rows of query head h read K/V head h / test_group
   float alpha;
   const uint8_t* q8_train;
   const uint8_t* q8_test;
@@ -38,6 +41,7 @@ struct Fp8Args {
   const float* s_q;
   const float* s_k;
   const float* s_v;
+  const float* s_q_test;
   void* o_train;
   void* o_test;
 };
@@ -118,19 +122,23 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   const int N = a.N, M = a.M;
   const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
   const int ql = lane % 32, half = lane / 32;
-  const int row = tile * kRowsPerBlock + wave * kRowsPerWave + ql;   // in [0, N+M)
+  // a workgroup serves either train rows (train-train call) or test rows (test-train call)
+  const bool test = tile >= a.tiles_train;
+  const int rows = test ? M : N;
+  const int row = (test ? tile - a.tiles_train : tile) * kRowsPerBlock + wave * kRowsPerWave + ql;
+  const int bhkv = test ? b * a.H + h / a.test_group : bh;   // the (b, K/V head) the rows attend to
 
   // Q_8 fragment: lane holds head_dim bytes [64s + 32*half, +32) of its row
   v8i qf[KD];
   {
-    const uint8_t* qrow = nullptr;
-    if (row < N) qrow = a.q8_train + ((size_t)bh * N + row) * D;
-    else if (row < N + M) qrow = a.q8_test + ((size_t)bh * M + (row - N)) * D;
+    const uint8_t* qrow = row < rows ? (test ? a.q8_test + ((size_t)bh * M + row) * D
+                                             : a.q8_train + ((size_t)bh * N + row) * D)
+                                     : nullptr;
 #pragma unroll
     for (int s = 0; s < KD; ++s) qf[s] = qrow ? load32(qrow + 64 * s + 32 * half) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
   }
-  const float c = a.alpha * a.s_q[bh] * a.s_k[bh] * kLog2e;
-  const float sv = a.s_v[bh];
+  const float c = a.alpha * (test ? a.s_q_test[bh] : a.s_q[bh]) * a.s_k[bhkv] * kLog2e;
+  const float sv = a.s_v[bhkv];
 
   // constant operand of the row-sum MFMA (see the header comment)
   v8i ones;
@@ -149,8 +157,8 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
 
   const int ntiles64 = (N + 63) / 64;
   const int nblocks = (N + BKV - 1) / BKV;
-  const uint8_t* kbase = a.k8 + (size_t)bh * N * D;
-  const uint8_t* vbase = a.v8t + (size_t)bh * ntiles64 * D * 64;
+  const uint8_t* kbase = a.k8 + (size_t)bhkv * N * D;
+  const uint8_t* vbase = a.v8t + (size_t)bhkv * ntiles64 * D * 64;
 
   u32x4 kr[PIECES], vr[PIECES];
   stage_load<D, BKV>(kbase, vbase, 0, N, ntiles64, kr, vr);
@@ -234,10 +242,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   }
 
   // ---- epilogue: O * s_v / l ----
-  if (row >= N + M) return;
+  if (row >= rows) return;
   const float inv = sv / lacc[0];
-  const size_t orow = row < N ? (((size_t)b * N + row) * a.H + h) * D
-                              : (((size_t)b * M + (row - N)) * a.H + h) * D;
+  const size_t orow = (((size_t)b * rows + row) * a.H + h) * D;
 #pragma unroll
   for (int i = 0; i < D / 32; ++i) {
 #pragma unroll
@@ -246,11 +253,11 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
       const float o0 = acc_o[i][4 * g + 0] * inv, o1 = acc_o[i][4 * g + 1] * inv;
       const float o2 = acc_o[i][4 * g + 2] * inv, o3 = acc_o[i][4 * g + 3] * inv;
       if constexpr (OUT_BF16) {
-        __bf16* op = (row < N ? (__bf16*)a.o_train : (__bf16*)a.o_test) + orow + d;
+        __bf16* op = (test ? (__bf16*)a.o_test : (__bf16*)a.o_train) + orow + d;
         typedef __bf16 v4bf __attribute__((ext_vector_type(4)));
         *reinterpret_cast<v4bf*>(op) = v4bf{(__bf16)o0, (__bf16)o1, (__bf16)o2, (__bf16)o3};
       } else {
-        float* op = (row < N ? (float*)a.o_train : (float*)a.o_test) + orow + d;
+        float* op = (test ? (float*)a.o_test : (float*)a.o_train) + orow + d;
         *reinterpret_cast<v4f*>(op) = v4f{o0, o1, o2, o3};
       }
     }
@@ -259,15 +266,18 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
 
 }  // namespace
 
-hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, float alpha, const uint8_t* q8_train,
-                           const uint8_t* q8_test, const uint8_t* k8, const uint8_t* v8t, const float* s_q,
-                           const float* s_k, const float* s_v, void* o_train, void* o_test, hipStream_t s) {
+hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads, float alpha,
+                           const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8, const uint8_t* v8t,
+                           const float* s_q, const float* s_k, const float* s_v, const float* s_q_test,
+                           void* o_train, void* o_test, hipStream_t s) {
   Fp8Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
-  a.tiles = (N + M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.tiles_train = (N + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.tiles = a.tiles_train + (M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.test_group = H / test_kv_heads;
   a.alpha = alpha;
   a.q8_train = q8_train; a.q8_test = q8_test; a.k8 = k8; a.v8t = v8t;
-  a.s_q = s_q; a.s_k = s_k; a.s_v = s_v; a.o_train = o_train; a.o_test = o_test;
+  a.s_q = s_q; a.s_k = s_k; a.s_v = s_v; a.s_q_test = s_q_test; a.o_train = o_train; a.o_test = o_test;
   dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
   if (D == 64) {
     if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, true>), grid, block, 0, s, a);

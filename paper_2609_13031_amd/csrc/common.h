@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/tfm.h"
+
 namespace tfm {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
@@ -23,8 +25,8 @@ constexpr float kLog2e = 1.4426950408889634f;
 
 // Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).
 struct Fp8Workspace {
-  size_t amax;      // 3*B*H uint32: |x| maxima of Q_train, K, V as float bits
-  size_t scales;    // 3*B*H float: s_q, s_k, s_v
+  size_t amax;      // 4*B*H uint32: |x| maxima of Q_train, K, V, Q_test as float bits
+  size_t scales;    // 4*B*H float: s_q, s_k, s_v, s_q_test
   size_t q8_train;  // (B,H,N,D) codes
   size_t q8_test;   // (B,H,M,D) codes
   size_t k8;        // (B,H,N,D) codes
@@ -37,13 +39,16 @@ size_t v8t_bytes(int B, int H, int D, int N);
 // ---- launchers (return hipError_t of the launches) ----
 // Zero `n` uint32 words.
 hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s);
-// Per-(b,h) absmax of Q_train, K, V into amax[3][B][H] (must be zeroed first).
-hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, const void* q_train,
-                       const void* k, const void* v, uint32_t* amax, hipStream_t s);
-// Scales from amax: s = fl32(amax/448), 1 where that is 0; writes scales[3][B][H]
-// and, when the pointers are non-NULL, copies to s_q/s_k/s_v.
-hipError_t launch_scales(int BH, const uint32_t* amax, float* scales, float* s_q, float* s_k,
-                         float* s_v, hipStream_t s);
+// Per-(b,h) absmax of Q_train, K, V (and of Q_test when q_test is non-NULL and
+// M > 0) into amax[4][B][H] (must be zeroed first).
+hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, int M, const void* q_train,
+                       const void* k, const void* v, const void* q_test, uint32_t* amax,
+                       hipStream_t s);
+// Scales from amax for a query-scale mode: s = fl32(amax/448), 1 where that is
+// 0; writes scales[4][B][H] (s_q, s_k, s_v, s_q_test) and, when the pointers are
+// non-NULL, copies them out.
+hipError_t launch_scales(int BH, int q_scale_mode, const uint32_t* amax, float* scales, float* s_q,
+                         float* s_k, float* s_v, float* s_q_test, hipStream_t s);
 // Quantize one (B,rows,H,D) tensor with per-(b,h) scales into (B,H,rows,D) codes.
 hipError_t launch_quantize_rows(int in_bf16, int B, int H, int D, int rows, const void* x,
                                 const float* scale, uint8_t* codes, hipStream_t s);
@@ -53,13 +58,15 @@ hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, cons
 // Re-lay (B,H,N,D) V codes into the tile-transposed layout.
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8,
                                    uint8_t* v8t, hipStream_t s);
-// Fused FP8 attention over the N+M query rows of every (b,h).
-hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, float alpha,
-                           const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8,
-                           const uint8_t* v8t, const float* s_q, const float* s_k,
-                           const float* s_v, void* o_train, void* o_test, hipStream_t s);
+// Fused FP8 attention over the N train and M test query rows of every (b,h).
+hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads,
+                           float alpha, const uint8_t* q8_train, const uint8_t* q8_test,
+                           const uint8_t* k8, const uint8_t* v8t, const float* s_q,
+                           const float* s_k, const float* s_v, const float* s_q_test,
+                           void* o_train, void* o_test, hipStream_t s);
 // bf16 baseline attention over the N+M query rows of every (b,h); fp32 inputs are rounded to bf16.
-hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, float alpha,
+hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads,
+                            float alpha,
                             const void* q_train, const void* q_test, const void* k,
                             const void* v, void* o_train, void* o_test, hipStream_t s);
 

@@ -78,13 +78,16 @@ struct RowMap {
 };
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void amax_kernel(int B, int H, int D, int N, int rows_per_chunk,
+__global__ __launch_bounds__(kThreads) void amax_kernel(int B, int H, int D, int N, int M, int rows_per_chunk,
                                                         const T* __restrict__ q, const T* __restrict__ k,
-                                                        const T* __restrict__ v, uint32_t* __restrict__ amax) {
+                                                        const T* __restrict__ v, const T* __restrict__ qt,
+                                                        uint32_t* __restrict__ amax) {
   extern __shared__ uint32_t smax[];  // H entries
   constexpr int VEC = Vec<T>::n;
   const int tensor = blockIdx.y, b = blockIdx.z;
-  const T* x = tensor == 0 ? q : (tensor == 1 ? k : v);
+  const T* x = tensor == 0 ? q : (tensor == 1 ? k : (tensor == 2 ? v : qt));
+  if (tensor == 3) N = M;   // the test queries have M rows
+  if ((int)blockIdx.x * rows_per_chunk >= N) return;
   for (int i = threadIdx.x; i < H; i += kThreads) smax[i] = 0;
   __syncthreads();
   const RowMap rm(H, D, VEC);
@@ -113,15 +116,26 @@ __global__ void fill_zero_kernel(uint32_t* p, int n) {
   if (i < n) p[i] = 0u;
 }
 
-__global__ void scales_kernel(int BH, const uint32_t* __restrict__ amax, float* __restrict__ scales,
-                              float* s_q, float* s_k, float* s_v) {
+// s = fl32(amax / 448), 1 where that is 0.  scales[4][BH] = s_q (train), s_k, s_v,
+// s_q_test.  Query-scale modes: shared -> s_q_test = s_q; per call -> each from
+// its own rows; joint -> both from the max over train and test rows.
+__device__ inline float scale_of(uint32_t amax_bits) {
+  float s = __uint_as_float(amax_bits) / 448.0f;
+  return s == 0.0f ? 1.0f : s;
+}
+__global__ void scales_kernel(int BH, int q_scale_mode, const uint32_t* __restrict__ amax, float* __restrict__ scales,
+                              float* s_q, float* s_k, float* s_v, float* s_q_test) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= 3 * BH) return;
-  float s = __uint_as_float(amax[i]) / 448.0f;
-  if (s == 0.0f) s = 1.0f;
-  scales[i] = s;
-  float* dst = i < BH ? s_q : (i < 2 * BH ? s_k : s_v);
-  if (dst) dst[i % BH] = s;
+  if (i >= BH) return;
+  const uint32_t aq = amax[i], aqt = amax[3 * BH + i];
+  const float sq = scale_of(q_scale_mode == TFM_QSCALE_JOINT ? max(aq, aqt) : aq);
+  const float sqt = q_scale_mode == TFM_QSCALE_PER_CALL ? scale_of(aqt) : sq;
+  const float sk = scale_of(amax[BH + i]), sv = scale_of(amax[2 * BH + i]);
+  scales[i] = sq; scales[BH + i] = sk; scales[2 * BH + i] = sv; scales[3 * BH + i] = sqt;
+  if (s_q) s_q[i] = sq;
+  if (s_k) s_k[i] = sk;
+  if (s_v) s_v[i] = sv;
+  if (s_q_test) s_q_test[i] = sqt;
 }
 
 template <typename T>
@@ -236,25 +250,28 @@ hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, const void* q_train, const void* k,
-                       const void* v, uint32_t* amax, hipStream_t s) {
+hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, int M, const void* q_train, const void* k,
+                       const void* v, const void* q_test, uint32_t* amax, hipStream_t s) {
   const int esize = in_bf16 ? 2 : 4;
+  const int rows = M > N ? M : N;
   const int rpc = chunk_rows(N, H, D, esize);
-  dim3 grid((N + rpc - 1) / rpc, 3, B);
+  // tensors 0..2 (Q_train, K, V) always; tensor 3 (Q_test) only when its max is needed
+  dim3 grid((rows + rpc - 1) / rpc, (q_test && M > 0) ? 4 : 3, B);
   size_t lds = (size_t)H * sizeof(uint32_t);
   if (in_bf16)
-    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, B, H, D, N, rpc,
-                       (const uint16_t*)q_train, (const uint16_t*)k, (const uint16_t*)v, amax);
+    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, B, H, D, N, M, rpc,
+                       (const uint16_t*)q_train, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)q_test,
+                       amax);
   else
-    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, B, H, D, N, rpc,
-                       (const float*)q_train, (const float*)k, (const float*)v, amax);
+    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, B, H, D, N, M, rpc, (const float*)q_train,
+                       (const float*)k, (const float*)v, (const float*)q_test, amax);
   return hipGetLastError();
 }
 
-hipError_t launch_scales(int BH, const uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
-                         hipStream_t s) {
-  hipLaunchKernelGGL(scales_kernel, dim3((3 * BH + 255) / 256), dim3(256), 0, s, BH, amax, scales, s_q, s_k,
-                     s_v);
+hipError_t launch_scales(int BH, int q_scale_mode, const uint32_t* amax, float* scales, float* s_q, float* s_k,
+                         float* s_v, float* s_q_test, hipStream_t s) {
+  hipLaunchKernelGGL(scales_kernel, dim3((BH + 255) / 256), dim3(256), 0, s, BH, q_scale_mode, amax, scales, s_q,
+                     s_k, s_v, s_q_test);
   return hipGetLastError();
 }
 

@@ -19,24 +19,41 @@ TFM_F32 = 0
 TFM_BF16 = 1
 _DTYPES = {torch.float32: TFM_F32, torch.bfloat16: TFM_BF16}
 
+# Query-scale modes of tfm_icl_options.q_scale_mode.
+Q_SCALE_MODES = {"shared": 0, "per_call": 1, "joint": 2}
+
+
+class tfm_icl_options(ctypes.Structure):
+    _fields_ = [("q_scale_mode", ctypes.c_int), ("test_kv_heads", ctypes.c_int)]
+
+
+def _opts(q_scale_mode="shared", test_kv_heads=0):
+    """A tfm_icl_options by reference; an unknown mode name raises ValueError here,
+    anything else the library checks."""
+    if q_scale_mode not in Q_SCALE_MODES:
+        raise ValueError("q_scale_mode must be one of %s" % sorted(Q_SCALE_MODES))
+    return ctypes.byref(tfm_icl_options(Q_SCALE_MODES[q_scale_mode], int(test_kv_heads or 0)))
+
 # name -> (restype, argtypes), in the order of include/tfm.h
 _c_int, _c_size, _c_float, _p = ctypes.c_int, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
+_o = ctypes.POINTER(tfm_icl_options)
 SIGNATURES = {
     "tfm_status_string": (ctypes.c_char_p, [_c_int]),
     "tfm_version": (_c_int, []),
     "tfm_quantize_workspace_bytes": (_c_size, [_c_int, _c_int]),
-    "tfm_quantize_qkv_per_head": (_c_int, [_c_int] * 6 + [_p] * 12 + [_c_size, _p]),
+    "tfm_quantize_qkv_per_head": (_c_int, [_c_int, _o] + [_c_int] * 5 + [_p] * 13 + [_c_size, _p]),
     "tfm_icl_attention_fp8_workspace_bytes": (_c_size, [_c_int] * 5),
-    "tfm_icl_attention_fp8": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 7 + [_c_size, _p]),
-    "tfm_icl_attention_fp8_quantize": (_c_int, [_c_int] * 6 + [_p] * 5 + [_c_size, _p]),
-    "tfm_icl_attention_fp8_attend": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 3 + [_c_size, _p]),
+    "tfm_icl_attention_fp8": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 7 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_quantize": (_c_int, [_c_int, _o] + [_c_int] * 5 + [_p] * 5 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_attend": (_c_int, [_c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 3 + [_c_size, _p]),
     "tfm_icl_attention_fp8_prequantized_workspace_bytes": (_c_size, [_c_int] * 4),
-    "tfm_icl_attention_fp8_prequantized": (_c_int, [_c_int] * 6 + [_c_float] + [_p] * 10 + [_c_size, _p]),
+    "tfm_icl_attention_fp8_prequantized": (_c_int, [_c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 11
+                                           + [_c_size, _p]),
     "tfm_icl_attention_fp8_block_kv": (_c_int, [_c_int]),
-    "tfm_icl_attention_bf16": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 6 + [_p]),
+    "tfm_icl_attention_bf16": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6 + [_p]),
     "tfm_icl_attention_workspace_bytes": (_c_size, [_c_int] * 6),
-    "tfm_icl_attention": (_c_int, [_c_int] * 7 + [_c_float] + [_p] * 6 + [_c_int, ctypes.POINTER(_c_int), _p,
-                                                                          _c_size, _p]),
+    "tfm_icl_attention": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6
+                          + [_c_int, ctypes.POINTER(_c_int), _p, _c_size, _p]),
 }
 
 
@@ -139,8 +156,9 @@ def tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N):
     return lib().tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
 
 
-def tfm_quantize_qkv_per_head(q_train, k, v, q_test=None):
-    """Eq. (2) per (b, h): returns dict q8_train, k8, v8, q8_test ((B,H,rows,D) uint8) and s_q, s_k, s_v ((B,H) fp32)."""
+def tfm_quantize_qkv_per_head(q_train, k, v, q_test=None, q_scale_mode="shared"):
+    """Eq. (2) per (b, h): returns dict q8_train, k8, v8, q8_test ((B,H,rows,D) uint8) and s_q, s_k, s_v,
+    s_q_test ((B,H) fp32; s_q_test is the scale the test queries were quantized with)."""
     B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
     if q_train.dtype not in _DTYPES:
         raise ValueError("inputs must be float32 or bfloat16")
@@ -151,12 +169,14 @@ def tfm_quantize_qkv_per_head(q_train, k, v, q_test=None):
            "q8_test": torch.empty((B, H, M, D), **u8) if M else None,
            "s_q": torch.empty((B, H), dtype=torch.float32, device=dev),
            "s_k": torch.empty((B, H), dtype=torch.float32, device=dev),
-           "s_v": torch.empty((B, H), dtype=torch.float32, device=dev)}
+           "s_v": torch.empty((B, H), dtype=torch.float32, device=dev),
+           "s_q_test": torch.empty((B, H), dtype=torch.float32, device=dev)}
     nws = tfm_quantize_workspace_bytes(B, H)
     ws = torch.empty(nws, **u8)
-    _call("tfm_quantize_qkv_per_head", _DTYPES[q_train.dtype], B, H, D, N, M, _ptr(q_train), _ptr(k), _ptr(v),
-          _ptr(q_test), _ptr(out["q8_train"]), _ptr(out["k8"]), _ptr(out["v8"]), _ptr(out["q8_test"]),
-          _ptr(out["s_q"]), _ptr(out["s_k"]), _ptr(out["s_v"]), _ptr(ws), nws, _stream())
+    _call("tfm_quantize_qkv_per_head", _DTYPES[q_train.dtype], _opts(q_scale_mode), B, H, D, N, M, _ptr(q_train),
+          _ptr(k), _ptr(v), _ptr(q_test), _ptr(out["q8_train"]), _ptr(out["k8"]), _ptr(out["v8"]),
+          _ptr(out["q8_test"]), _ptr(out["s_q"]), _ptr(out["s_k"]), _ptr(out["s_v"]), _ptr(out["s_q_test"]),
+          _ptr(ws), nws, _stream())
     if out["q8_test"] is None:
         out["q8_test"] = torch.empty((B, H, 0, D), **u8)
     return out
@@ -176,8 +196,13 @@ def _outputs(B, H, D, N, M, out_dtype, dev, out):
     return o_tr, o_te
 
 
-def tfm_icl_attention_fp8(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None, workspace=None):
-    """Quantize (Eq. (2)) and run both ICL calls in FP8; returns (o_train (B,N,H,D), o_test (B,M,H,D))."""
+def tfm_icl_attention_fp8(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None, workspace=None,
+                          q_scale_mode="shared", test_kv_heads=0):
+    """Quantize (Eq. (2)) and run both ICL calls in FP8; returns (o_train (B,N,H,D), o_test (B,M,H,D)).
+
+    q_scale_mode: "shared" (test queries on the train-query scale), "per_call" (their own
+    scale) or "joint" (one scale over train and test queries).  test_kv_heads G (0 = H):
+    test queries of head h attend to K/V head h // (H // G)."""
     B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
     if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
         raise ValueError("inputs and outputs must be float32 or bfloat16")
@@ -185,13 +210,14 @@ def tfm_icl_attention_fp8(q_train, k, v, q_test=None, alpha=None, out_dtype=torc
     o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
     nws = tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
     ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
-    _call("tfm_icl_attention_fp8", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+    _call("tfm_icl_attention_fp8", _DTYPES[q_train.dtype], _DTYPES[out_dtype], _opts(q_scale_mode, test_kv_heads),
+          B, H, D, N, M, _alpha(alpha, D),
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _ptr(ws),
           ws.numel(), _stream())
     return o_tr, o_te
 
 
-def tfm_icl_attention_fp8_quantize(q_train, k, v, q_test=None, workspace=None):
+def tfm_icl_attention_fp8_quantize(q_train, k, v, q_test=None, workspace=None, q_scale_mode="shared"):
     """First stage of tfm_icl_attention_fp8: quantize into a workspace (returned)."""
     B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
     if q_train.dtype not in _DTYPES:
@@ -199,51 +225,59 @@ def tfm_icl_attention_fp8_quantize(q_train, k, v, q_test=None, workspace=None):
     dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
     nws = tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M)
     ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
-    _call("tfm_icl_attention_fp8_quantize", _DTYPES[q_train.dtype], B, H, D, N, M, _ptr(q_train), _ptr(k), _ptr(v),
-          _ptr(q_test), _ptr(ws), ws.numel(), _stream())
+    _call("tfm_icl_attention_fp8_quantize", _DTYPES[q_train.dtype], _opts(q_scale_mode), B, H, D, N, M,
+          _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(ws), ws.numel(), _stream())
     return ws
 
 
-def tfm_icl_attention_fp8_attend(workspace, B, H, D, N, M, alpha=None, out_dtype=torch.float32, out=None):
+def tfm_icl_attention_fp8_attend(workspace, B, H, D, N, M, alpha=None, out_dtype=torch.float32, out=None,
+                                 test_kv_heads=0):
     """Second stage of tfm_icl_attention_fp8: both ICL calls from a quantized workspace."""
     if out_dtype not in _DTYPES:
         raise ValueError("outputs must be float32 or bfloat16")
     dev = _check_inputs({"workspace": workspace}, torch.uint8)
     o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
-    _call("tfm_icl_attention_fp8_attend", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D), _ptr(o_tr),
+    _call("tfm_icl_attention_fp8_attend", _DTYPES[out_dtype], _opts("shared", test_kv_heads), B, H, D, N, M,
+          _alpha(alpha, D), _ptr(o_tr),
           _ptr(o_te if M else None), _ptr(workspace), workspace.numel(), _stream())
     return o_tr, o_te
 
 
 def tfm_icl_attention_fp8_prequantized(q8_train, k8, v8, q8_test, s_q, s_k, s_v, alpha=None,
-                                       out_dtype=torch.float32, out=None, workspace=None):
-    """Both ICL calls on codes/scales from tfm_quantize_qkv_per_head; returns (o_train, o_test)."""
+                                       out_dtype=torch.float32, out=None, workspace=None, s_q_test=None,
+                                       test_kv_heads=0):
+    """Both ICL calls on codes/scales from tfm_quantize_qkv_per_head; returns (o_train, o_test).
+
+    s_q_test (None = s_q) is the scale of the test-query codes."""
     B, H, N, D = q8_train.shape
     M = 0 if q8_test is None else q8_test.shape[2]
     if M == 0:
         q8_test = None
     dev = _check_inputs({"q8_train": q8_train, "k8": k8, "v8": v8, "q8_test": q8_test}, torch.uint8)
-    _check_inputs({"s_q": s_q, "s_k": s_k, "s_v": s_v}, torch.float32)
+    _check_inputs({"s_q": s_q, "s_k": s_k, "s_v": s_v, "s_q_test": s_q_test}, torch.float32)
     for name, t in (("k8", k8), ("v8", v8)):
         if tuple(t.shape) != (B, H, N, D):
             raise ValueError("%s must be (B, H, N, D)" % name)
     o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
     nws = tfm_icl_attention_fp8_prequantized_workspace_bytes(B, H, D, N)
     ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
-    _call("tfm_icl_attention_fp8_prequantized", _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
-          _ptr(q8_train), _ptr(k8), _ptr(v8), _ptr(q8_test), _ptr(s_q), _ptr(s_k), _ptr(s_v), _ptr(o_tr),
+    _call("tfm_icl_attention_fp8_prequantized", _DTYPES[out_dtype], _opts("shared", test_kv_heads), B, H, D, N, M,
+          _alpha(alpha, D), _ptr(q8_train), _ptr(k8), _ptr(v8), _ptr(q8_test), _ptr(s_q), _ptr(s_k), _ptr(s_v),
+          _ptr(s_q_test), _ptr(o_tr),
           _ptr(o_te if M else None), _ptr(ws), ws.numel(), _stream())
     return o_tr, o_te
 
 
-def tfm_icl_attention_bf16(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None):
+def tfm_icl_attention_bf16(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None,
+                           test_kv_heads=0):
     """The 16-bit baseline of both ICL calls (bf16, or fp32 rounded to bf16 on load); returns (o_train, o_test)."""
     B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
     if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
         raise ValueError("inputs and outputs must be float32 or bfloat16")
     dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
     o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
-    _call("tfm_icl_attention_bf16", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+    _call("tfm_icl_attention_bf16", _DTYPES[q_train.dtype], _DTYPES[out_dtype], _opts("shared", test_kv_heads),
+          B, H, D, N, M, _alpha(alpha, D),
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
     return o_tr, o_te
 
@@ -252,7 +286,7 @@ FP8_MIN_TRAIN_ROWS_DEFAULT = 8192
 
 
 def tfm_icl_attention(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, fp8_min_train_rows=-1,
-                      out=None, workspace=None):
+                      out=None, workspace=None, q_scale_mode="shared", test_kv_heads=0):
     """Gated ICL attention: FP8 when N > fp8_min_train_rows (default 8192), else the 16-bit path.
 
     Returns (o_train, o_test, used_fp8)."""
@@ -264,7 +298,8 @@ def tfm_icl_attention(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.fl
     nws = lib().tfm_icl_attention_workspace_bytes(B, H, D, N, M, int(fp8_min_train_rows))
     ws = workspace if workspace is not None else (torch.empty(nws, dtype=torch.uint8, device=dev) if nws else None)
     used = ctypes.c_int(-1)
-    _call("tfm_icl_attention", _DTYPES[q_train.dtype], _DTYPES[out_dtype], B, H, D, N, M, _alpha(alpha, D),
+    _call("tfm_icl_attention", _DTYPES[q_train.dtype], _DTYPES[out_dtype], _opts(q_scale_mode, test_kv_heads),
+          B, H, D, N, M, _alpha(alpha, D),
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None),
           int(fp8_min_train_rows), ctypes.byref(used), _ptr(ws), 0 if ws is None else ws.numel(), _stream())
     return o_tr, o_te, bool(used.value)

@@ -80,11 +80,16 @@ def p_rounding_bound(q8, k8, v_hat, c, eps_dot=0.0, n_tiles=0):
     return o, bound
 
 
-def assert_t2(got, qz, alpha, b, h, q8_rows, slack=1.25, eps_dot=EPS_DOT):
-    """T2': |O_gpu - O_q| <= 1.25 * p_rounding_bound(eps_dot) + 1e-5 * RMS, elementwise."""
-    c = float(alpha) * float(qz["s_q"][b, h]) * float(qz["s_k"][b, h]) * OA.LOG2E
-    k8 = decode(qz["k8"][b, h])
-    v_hat = decode(qz["v8"][b, h]) * float(qz["s_v"][b, h])
+def assert_t2(got, qz, alpha, b, h, q8_rows, slack=1.25, eps_dot=EPS_DOT, s_query=None, hk=None):
+    """T2': |O_gpu - O_q| <= 1.25 * p_rounding_bound(eps_dot) + 1e-5 * RMS, elementwise.
+
+    The query rows q8_rows have scale s_query (default s_q of head h) and attend to K/V
+    head hk (default h)."""
+    hk = h if hk is None else hk
+    s_query = qz["s_q"][b, h] if s_query is None else s_query
+    c = float(alpha) * float(s_query) * float(qz["s_k"][b, hk]) * OA.LOG2E
+    k8 = decode(qz["k8"][b, hk])
+    v_hat = decode(qz["v8"][b, hk]) * float(qz["s_v"][b, hk])
     n_tiles = (k8.shape[0] + 63) // 64
     o, bnd = p_rounding_bound(decode(q8_rows), k8, v_hat, c, eps_dot, n_tiles)
     rms = np.sqrt(np.mean(o ** 2))

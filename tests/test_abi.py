@@ -32,7 +32,7 @@ def test_status_strings_and_version():
     for st in range(1, 9):
         assert L.tfm_status_string(st).startswith(b"TFM_ERR_")
     assert L.tfm_status_string(99) == b"TFM_ERR_UNKNOWN"
-    assert tfm.tfm_version() == 100
+    assert tfm.tfm_version() == 200
 
 
 def test_block_kv_and_workspace_queries():
@@ -41,7 +41,8 @@ def test_block_kv_and_workspace_queries():
     assert tfm.tfm_icl_attention_fp8_block_kv(96) == 0
     assert tfm.tfm_quantize_workspace_bytes(2, 6) == 512
     assert tfm.tfm_quantize_workspace_bytes(0, 6) == 0
-    # codes of Q_train, Q_test, K (N or M x D per head), V tiles (ceil(N/64)*64*D), amax, scales
+    # amax and scales (4*B*H words each, 256-aligned), codes of Q_train, Q_test, K (N or M x D per head),
+    # V tiles (ceil(N/64)*64*D)
     B, H, D, N, M = 2, 6, 64, 65536, 16384
     want = 256 + 256 + B * H * (N * D + M * D + N * D + N * D)
     assert tfm.tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M) == want
@@ -54,13 +55,17 @@ FAKE = 0x10000          # aligned, never dereferenced: every call below fails va
 MIS = 0x10008           # 8-byte aligned only
 
 
+def opts(mode=0, g=0):
+    return ctypes.byref(tfm.tfm_icl_options(mode, g))
+
+
 def fp8_call(**kw):
-    a = dict(in_dtype=1, out_dtype=0, B=1, H=2, D=64, N=100, M=10, alpha=0.125, q_train=FAKE, k=FAKE, v=FAKE,
-             q_test=FAKE, o_train=FAKE, o_test=FAKE, ws=FAKE, nws=1 << 40)
+    a = dict(in_dtype=1, out_dtype=0, opts=None, B=1, H=2, D=64, N=100, M=10, alpha=0.125, q_train=FAKE, k=FAKE,
+             v=FAKE, q_test=FAKE, o_train=FAKE, o_test=FAKE, ws=FAKE, nws=1 << 40)
     a.update(kw)
-    return tfm.lib().tfm_icl_attention_fp8(a["in_dtype"], a["out_dtype"], a["B"], a["H"], a["D"], a["N"], a["M"],
-                                           a["alpha"], a["q_train"], a["k"], a["v"], a["q_test"], a["o_train"],
-                                           a["o_test"], a["ws"], a["nws"], None)
+    return tfm.lib().tfm_icl_attention_fp8(a["in_dtype"], a["out_dtype"], a["opts"], a["B"], a["H"], a["D"], a["N"],
+                                           a["M"], a["alpha"], a["q_train"], a["k"], a["v"], a["q_test"],
+                                           a["o_train"], a["o_test"], a["ws"], a["nws"], None)
 
 
 @pytest.mark.parametrize("kw,status", [
@@ -71,6 +76,11 @@ def fp8_call(**kw):
     (dict(q_train=None), 1), (dict(k=None), 1), (dict(ws=None), 1), (dict(q_test=None), 1), (dict(o_test=None), 1),
     (dict(v=MIS), 5), (dict(o_train=MIS), 5), (dict(q_test=MIS), 5),
     (dict(nws=1000), 6),
+    (dict(opts=opts(mode=3)), 8), (dict(opts=opts(mode=-1)), 8), (dict(opts=opts(g=3, mode=1)), 8),
+    (dict(opts=opts(g=-1)), 8), (dict(opts=opts(g=4)), 8), (dict(H=6, opts=opts(g=4)), 8),
+    (dict(opts=opts(mode=3), q_train=None), 8),
+    (dict(opts=opts(mode=2, g=1), nws=1000), 6), (dict(H=6, opts=opts(mode=1, g=3), nws=1000), 6),
+    (dict(opts=opts(g=2), nws=1000), 6),
 ])
 def test_fp8_validation_errors(kw, status):
     assert fp8_call(**kw) == status
@@ -85,38 +95,42 @@ def test_validation_order_and_m_zero_allows_null_test_pointers():
 
 def test_quantize_and_bf16_and_prequantized_validation():
     L = tfm.lib()
-    q = lambda **kw: L.tfm_quantize_qkv_per_head(kw.get("dt", 0), kw.get("B", 1), 2, kw.get("D", 64), 50, 0,
-                                                 FAKE, FAKE, FAKE, None, FAKE, FAKE, kw.get("v8", FAKE), None,
-                                                 FAKE, FAKE, FAKE, FAKE, kw.get("nws", 1 << 20), None)
+    q = lambda **kw: L.tfm_quantize_qkv_per_head(kw.get("dt", 0), kw.get("o"), kw.get("B", 1), 2, kw.get("D", 64),
+                                                 50, 0, FAKE, FAKE, FAKE, None, FAKE, FAKE, kw.get("v8", FAKE), None,
+                                                 FAKE, FAKE, FAKE, kw.get("sqt"), FAKE, kw.get("nws", 1 << 20), None)
     assert q(dt=5) == 3 and q(B=0) == 2 and q(D=100) == 4 and q(v8=None) == 1 and q(v8=MIS) == 5 and q(nws=8) == 6
-    b = lambda **kw: L.tfm_icl_attention_bf16(kw.get("inp", 1), kw.get("out", 1), 1, 2, 64, kw.get("N", 50), 3,
-                                              kw.get("alpha", 0.1), FAKE, FAKE, FAKE, kw.get("qt", FAKE), FAKE, FAKE,
-                                              None)
+    assert q(o=opts(mode=5)) == 8 and q(o=opts(g=3)) == 8 and q(sqt=MIS) == 5 and q(sqt=FAKE, nws=8) == 6
+    assert q(o=opts(mode=1, g=1), nws=8) == 6
+    b = lambda **kw: L.tfm_icl_attention_bf16(kw.get("inp", 1), kw.get("out", 1), kw.get("o"), 1, 2, 64,
+                                              kw.get("N", 50), 3, kw.get("alpha", 0.1), FAKE, FAKE, FAKE,
+                                              kw.get("qt", FAKE), FAKE, FAKE, None)
     assert b(out=3) == 3 and b(inp=4) == 3 and b(N=0) == 2 and b(alpha=-2.0) == 8 and b(qt=None) == 1
-    assert b(qt=MIS) == 5
-    qs = lambda **kw: L.tfm_icl_attention_fp8_quantize(1, 1, 2, 64, 50, kw.get("M", 3), FAKE, FAKE, FAKE,
-                                                       kw.get("qt", FAKE), FAKE, kw.get("nws", 1 << 30), None)
-    assert qs(qt=None) == 1 and qs(M=0, qt=None, nws=10) == 6 and qs(qt=MIS) == 5
-    at = lambda **kw: L.tfm_icl_attention_fp8_attend(0, 1, 2, 64, 50, 3, kw.get("alpha", 0.1), FAKE,
+    assert b(qt=MIS) == 5 and b(o=opts(g=3)) == 8 and b(o=opts(g=1), qt=None) == 1
+    qs = lambda **kw: L.tfm_icl_attention_fp8_quantize(1, kw.get("o"), 1, 2, 64, 50, kw.get("M", 3), FAKE, FAKE,
+                                                       FAKE, kw.get("qt", FAKE), FAKE, kw.get("nws", 1 << 30), None)
+    assert qs(qt=None) == 1 and qs(M=0, qt=None, nws=10) == 6 and qs(qt=MIS) == 5 and qs(o=opts(mode=9)) == 8
+    at = lambda **kw: L.tfm_icl_attention_fp8_attend(0, kw.get("o"), 1, 2, 64, 50, 3, kw.get("alpha", 0.1), FAKE,
                                                      kw.get("ot", FAKE), FAKE, kw.get("nws", 1 << 30), None)
-    assert at(alpha=0.0) == 8 and at(ot=None) == 1 and at(nws=1) == 6
-    p = lambda **kw: L.tfm_icl_attention_fp8_prequantized(0, 1, 2, 64, 50, 0, 0.1, FAKE, FAKE, FAKE, None, FAKE,
-                                                          kw.get("sk", FAKE), FAKE, FAKE, None, FAKE,
-                                                          kw.get("nws", 1 << 20), None)
-    assert p(sk=None) == 1 and p(nws=100) == 6
+    assert at(alpha=0.0) == 8 and at(ot=None) == 1 and at(nws=1) == 6 and at(o=opts(g=5)) == 8
+    p = lambda **kw: L.tfm_icl_attention_fp8_prequantized(0, kw.get("o"), 1, 2, 64, 50, 0, 0.1, FAKE, FAKE, FAKE,
+                                                          None, FAKE, kw.get("sk", FAKE), FAKE, kw.get("sqt"),
+                                                          FAKE, None, FAKE, kw.get("nws", 1 << 20), None)
+    assert p(sk=None) == 1 and p(nws=100) == 6 and p(o=opts(g=3)) == 8 and p(sqt=MIS) == 5
 
 
 def test_gate_selects_the_path_before_validating_it():
     L = tfm.lib()
     used = ctypes.c_int(-7)
-    g = lambda N, gate, **kw: L.tfm_icl_attention(1, 1, 1, 2, 64, N, 3, 0.1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, gate,
-                                                  ctypes.byref(used), kw.get("ws", FAKE), kw.get("nws", 0), None)
+    g = lambda N, gate, **kw: L.tfm_icl_attention(1, 1, kw.get("o"), 1, 2, 64, N, 3, 0.1, FAKE, FAKE, FAKE, FAKE,
+                                                  FAKE, FAKE, gate, ctypes.byref(used), kw.get("ws", FAKE),
+                                                  kw.get("nws", 0), None)
     # The FP8 path needs a workspace, the 16-bit path none: the reported error
     # tells which one validated.  (Every call here must fail validation: the
     # pointers are fake and must never reach a kernel.)
     assert g(8193, -1) == 6 and g(9000, 8192) == 6 and g(100, 50) == 6
-    assert L.tfm_icl_attention(1, 1, 1, 2, 64, 8192, 3, 0.1, FAKE, FAKE, FAKE, None, FAKE, FAKE, -1,
+    assert L.tfm_icl_attention(1, 1, None, 1, 2, 64, 8192, 3, 0.1, FAKE, FAKE, FAKE, None, FAKE, FAKE, -1,
                                ctypes.byref(used), None, 0, None) == 1      # 16-bit path: NULL q_test with M > 0
+    assert g(8193, -1, o=opts(g=3)) == 8 and g(100, -1, o=opts(mode=4)) == 8
     assert used.value == -7                        # not written on failure
     assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 8192, 3, -1) == 0
     assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 8193, 3, -1) == tfm.tfm_icl_attention_fp8_workspace_bytes(

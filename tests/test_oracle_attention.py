@@ -191,3 +191,64 @@ def test_tie_allowance_bounds_the_effect_of_perturbed_exponents():
     # with a tiny window nothing is flagged in a generic row
     _, allow0 = A.one_pass_fp8_attention(q8[:3], k8, v8, c, 0.01, N, tie_rel=1e-15)
     assert allow0.max() < 1e-9 * np.abs(o).max()
+
+
+def _repeat_heads(x, H, G, axis):
+    """The standard grouped-query expansion: head h of the result is head h // (H // G) of x."""
+    return np.repeat(np.take(x, np.arange(G), axis=axis), H // G, axis=axis)
+
+
+@pytest.mark.parametrize("G", [1, 2, 4])
+def test_grouped_test_heads_equal_attention_over_repeated_kv_heads(G):
+    # Appendix (noise experiment): TabPFN-v3's test rows attend, grouped-query style, to the
+    # first K/V head(s) of the train-train call.
+    qt, k, v, qe = _small_qkv(21, B=2, N=150, M=20, H=4)
+    o_tr, o_te = A.icl_attention(qt, k, v, qe, 0.125, test_kv_heads=G)
+    ref_tr, _ = A.icl_attention(qt, k, v, qe, 0.125)
+    _, ref_te = A.icl_attention(qt, _repeat_heads(k, 4, G, 2), _repeat_heads(v, 4, G, 2), qe, 0.125)
+    assert np.allclose(o_tr, ref_tr, rtol=0, atol=1e-13)
+    assert np.allclose(o_te, ref_te, rtol=0, atol=1e-13)
+    # the FP8 kernel model reads that K/V head's codes and scales for the test rows
+    qz = Q.quantize_qkv_per_head(qt, k, v, qe)
+    rep = dict(qz)
+    for key in ("k8", "v8", "s_k", "s_v"):
+        rep[key] = _repeat_heads(qz[key], 4, G, 1)
+    m_tr, m_te = A.icl_attention_fp8_kernel_model(qz, 0.125, 64, test_kv_heads=G)
+    r_tr, _ = A.icl_attention_fp8_kernel_model(qz, 0.125, 64)
+    _, r_te = A.icl_attention_fp8_kernel_model(rep, 0.125, 64)
+    assert np.array_equal(m_tr, r_tr) and np.array_equal(m_te, r_te)
+    d_tr, d_te = A.icl_attention_dequantized(qz, 0.125, test_kv_heads=G)
+    _, e_te = A.icl_attention_dequantized(rep, 0.125)
+    assert np.allclose(d_te, e_te, rtol=0, atol=1e-13)
+    if G < 4:
+        assert not np.allclose(o_te, A.icl_attention(qt, k, v, qe, 0.125)[1], atol=1e-3)
+
+
+def test_grouped_test_heads_must_divide_h():
+    qt, k, v, qe = _small_qkv(22, N=10, M=3, H=4)
+    with pytest.raises(ValueError):
+        A.icl_attention(qt, k, v, qe, 0.125, test_kv_heads=3)
+
+
+@pytest.mark.parametrize("mode,test_mult", [("per_call", 0.0625), ("joint", 2.0)])
+def test_kernel_model_uses_the_test_query_scale(mode, test_mult):
+    # per_call: test queries 16x below the train amax get a scale ~16x below s_q, so a test
+    # call that used s_q for them would scale its logits by ~16.  joint: test queries above the
+    # train amax set the one scale of both calls.
+    qt, k, v, qe = _small_qkv(23, N=300, M=24, spread=1.0)
+    qe = qe * np.float32(test_mult)
+    qz = Q.quantize_qkv_per_head(qt, k, v, qe, q_scale_mode=mode)
+    assert np.all(np.abs(qz["s_q_test"] / qz["s_q"] - test_mult) < 0.5 * test_mult) if mode == "per_call" else \
+        np.array_equal(qz["s_q_test"], qz["s_q"])
+    ex_tr, ex_te = A.icl_attention(qt, k, v, qe, 0.125)
+    o_tr, o_te = A.icl_attention_fp8_kernel_model(qz, 0.125, 64)
+    d_tr, d_te = A.icl_attention_dequantized(qz, 0.125)
+    for h in range(2):
+        c = 0.125 * float(qz["s_q_test"][0, h]) * float(qz["s_k"][0, h]) * A.LOG2E
+        kq, vq = decode(qz["k8"][0, h]), decode(qz["v8"][0, h]) * float(qz["s_v"][0, h])
+        o, bnd = p_rounding_bound(decode(qz["q8_test"][0, h]), kq, vq, c)
+        assert np.allclose(o, d_te[0, :, h], atol=1e-9 * np.abs(o).max())
+        assert np.all(np.abs(o_te[0, :, h] - d_te[0, :, h]) <= bnd * (1 + 1e-9) + 1e-12)
+    # and O_q and O_qp stay within the FP8 quantization error of the exact result on both calls
+    for got, ex in ((d_tr, ex_tr), (d_te, ex_te), (o_tr, ex_tr), (o_te, ex_te)):
+        assert np.linalg.norm(got - ex) / np.linalg.norm(ex) < 0.1      # a wrong query scale gives ~1

@@ -100,3 +100,67 @@ def test_layout_and_dequantization_error_bound():
     # half an e4m3 ulp: 2^-4 relative in the normal range, 2^-10 absolute below 2^-6 (+ fp32 division)
     bound = s[:, :, None, None] * (np.maximum(y * 2.0 ** -4, 2.0 ** -10) * (1 + 1e-6) + 1e-6 * y)
     assert np.all(np.abs(xhat - xt) <= bound)
+
+
+def test_per_call_test_scale_is_the_test_batch_absmax_and_couples_test_rows():
+    # Table 1, "per-call query scale": the test queries get a scale of their own.
+    x = _x((1, 300, 2, 64), 11)
+    q_test = _x((1, 50, 2, 64), 12) * np.float32(0.0625)           # far below the train amax
+    q_test[0, 9, 0, 7] = np.float32(3.0) * np.abs(q_test[0, :, 0, :]).max()
+    shared = Q.quantize_qkv_per_head(x, x, x, q_test)
+    per = Q.quantize_qkv_per_head(x, x, x, q_test, q_scale_mode="per_call")
+    for key in ("q8_train", "k8", "v8", "s_q", "s_k", "s_v"):
+        assert np.array_equal(per[key], shared[key])
+    assert np.array_equal(shared["s_q_test"], shared["s_q"])
+    # the test absmax element maps to 448 under its own scale, and no code saturates beyond it
+    dec = np.abs(decode(per["q8_test"]))
+    assert np.array_equal(dec.max(axis=(2, 3)), np.full((1, 2), 448.0))
+    assert per["q8_test"][0, 0, 9, 7] == 0x7E
+    assert not np.array_equal(per["s_q_test"], per["s_q"])
+    # scaling the test batch by a power of two leaves its codes unchanged
+    per4 = Q.quantize_qkv_per_head(x, x, x, q_test * np.float32(4.0), q_scale_mode="per_call")
+    assert np.array_equal(per4["q8_test"], per["q8_test"])
+    assert np.array_equal(per4["s_q_test"], per["s_q_test"] * np.float32(4.0))
+    # dropping the row that holds head 0's absmax changes the other rows' codes (Sec. 3: the
+    # per-call scale couples the test rows); the shared scale does not
+    keep = [r for r in range(50) if r != 9]
+    sub_per = Q.quantize_qkv_per_head(x, x, x, q_test[:, keep], q_scale_mode="per_call")
+    sub_sh = Q.quantize_qkv_per_head(x, x, x, q_test[:, keep])
+    assert not np.array_equal(sub_per["q8_test"][:, 0], per["q8_test"][:, 0][:, keep])
+    assert np.array_equal(sub_sh["q8_test"], shared["q8_test"][:, :, keep])
+
+
+def test_joint_scale_is_one_scale_over_train_and_test_queries():
+    # The single ICL call over all rows of the TabICLv2 experiments: one per-head scale over
+    # the union of the train and test query rows.
+    x = _x((2, 200, 3, 64), 13)
+    q_test = _x((2, 40, 3, 64), 14)
+    q_test[1, 3, 2, 5] = np.float32(6.0) * np.abs(x[1, :, 2, :]).max()   # head (1,2): test amax wins
+    joint = Q.quantize_qkv_per_head(x, x, x, q_test, q_scale_mode="joint")
+    assert np.array_equal(joint["s_q_test"], joint["s_q"])
+    both = np.concatenate([x, q_test], axis=1)
+    s = Q.scale_from_amax(Q.absmax_per_head(both))
+    codes = Q.quantize_with_scale(both, s)
+    assert np.array_equal(joint["s_q"], s)
+    assert np.array_equal(joint["q8_train"], codes[:, :, :200])
+    assert np.array_equal(joint["q8_test"], codes[:, :, 200:])
+    # where the train amax is the larger, joint and shared agree bit for bit
+    shared = Q.quantize_qkv_per_head(x, x, x, q_test)
+    at_train = np.abs(x).max(axis=(1, 3)) >= np.abs(q_test).max(axis=(1, 3))
+    assert at_train.sum() >= 3 and not at_train[1, 2]
+    for b, h in zip(*np.nonzero(at_train)):
+        assert np.array_equal(joint["q8_test"][b, h], shared["q8_test"][b, h])
+        assert joint["s_q"][b, h] == shared["s_q"][b, h]
+    # head (1,2): the shared scale saturates the large test value, the joint one does not clip it
+    assert shared["q8_test"][1, 2, 3, 5] == 0x7E and joint["q8_test"][1, 2, 3, 5] == 0x7E
+    assert (np.abs(decode(joint["q8_train"][1, 2])).max() < 448.0 / 4)
+    assert (np.abs(decode(shared["q8_train"][1, 2])).max() == 448.0)
+
+
+def test_unknown_query_scale_mode_is_rejected():
+    x = _x((1, 8, 1, 64), 15)
+    try:
+        Q.quantize_qkv_per_head(x, x, x, x, q_scale_mode="per_head")
+    except ValueError:
+        return
+    raise AssertionError("expected ValueError")
