@@ -151,6 +151,39 @@ def crossover(max_n):
     return {"crossover": rows, "call": "train-train only, B=1, H=8, bf16 in/out, FP8 time includes quantization"}
 
 
+def noise_op(w, steps, warmup):
+    """Eq. (3) on the K tensor of the workload (bf16 x, bf16 z), timed per call with HIP events on
+    the stream the library launches on; HBM roofline on the algorithmic bytes x + z + out."""
+    import torch
+    from paper_2609_13031_amd import tfm
+
+    shape = (w.B, w.N, w.H, w.D)
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    x = torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    z = torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
+    out = torch.empty_like(x)
+    ws = torch.empty(tfm.tfm_noise_per_head_workspace_bytes(w.B, w.H, w.N, w.D), dtype=torch.uint8, device="cuda")
+    run = lambda: tfm.tfm_noise_per_head(x, z, 0.0265, out=out, workspace=ws)
+    for _ in range(warmup):
+        run()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for _ in range(steps):
+        run()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / steps
+    algo = 3 * x.numel() * 2
+    gbs = algo / ms / 1e6
+    log("noise op %.4f ms, %.1f GB/s" % (ms, gbs))
+    return {"noise_op": {"tensor": "K of %s: (B=%d, S=%d, H=%d, D=%d) bf16, z bf16" % (w.name, *shape),
+                         "ms_per_call": round(ms, 4), "algorithmic_bytes": algo,
+                         "roofline": {"bound": "hbm", "achieved": round(gbs, 1), "peak": 8000.0, "unit": "GB/s",
+                                      "frac": round(gbs / 8000.0, 4)},
+                         "design_bytes": 4 * x.numel() * 2, "steps": steps, "warmup": warmup}}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -166,6 +199,9 @@ def main():
                     help="instead of the headline step: FP8 (quantization included) vs bf16 for one train-train "
                          "call, B=1, H=8, N=1k..512k, D=64 and 128; prints one JSON line with the table")
     ap.add_argument("--crossover-max-n", type=int, default=1 << 19)
+    ap.add_argument("--noise", action="store_true",
+                    help="instead of the headline step: the Eq. (3) noise operator on the workload's K tensor; "
+                         "prints one JSON line")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run a 1 GiB device copy (for scaling HBM counters)")
     args = ap.parse_args()
@@ -185,6 +221,9 @@ def main():
         print(json.dumps(crossover(args.crossover_max_n)), flush=True)
         return
     w = WORKLOADS[args.workload]
+    if args.noise:
+        print(json.dumps(noise_op(w, args.steps, args.warmup)), flush=True)
+        return
     log("generating", w)
     x = generate(w)
     in_dt = torch.float32 if w.dtype == "f32" else torch.bfloat16

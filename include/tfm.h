@@ -54,7 +54,7 @@ typedef enum {
   TFM_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
   TFM_ERR_WORKSPACE_TOO_SMALL = 6,  /* workspace_bytes below the size query */
   TFM_ERR_HIP = 7,                  /* the HIP runtime reported an error */
-  TFM_ERR_BAD_ARG = 8               /* alpha not finite and positive, or a bad option */
+  TFM_ERR_BAD_ARG = 8               /* alpha not finite and positive, eps not finite and >= 0, or a bad option */
 } tfm_status;
 
 typedef enum { TFM_F32 = 0, TFM_BF16 = 1 } tfm_dtype;
@@ -237,6 +237,40 @@ int tfm_icl_attention(int in_dtype, int out_dtype, const tfm_icl_options* opts, 
                       const void* q_train, const void* k, const void* v, const void* q_test,
                       void* o_train, void* o_test, int fp8_min_train_rows, int* used_fp8,
                       void* workspace, size_t workspace_bytes, tfm_stream stream);
+
+/*
+ * tfm_noise_per_head -- the per-head RMS-scaled Gaussian perturbation of
+ * Eq. (3) (appendix, noise experiment), the explicit stand-in for quantization
+ * error that the paper uses to study which calls may see perturbed inputs.
+ *
+ * For every table b and head h:
+ *   rho[b,h] = fl32( sqrt( sum over rows i < S, channels j < D of x^2 / (S*D) ) )
+ *   out      = fmaf( fl32(eps * rho[b,h]), z, x )         (one rounding in fp32)
+ * then converted to the type of x (bf16: round to nearest even).  The sum is
+ * taken in fp64 in a fixed order, so results are bitwise reproducible.  The
+ * random field z is an input: the caller draws it (standard normal, from its
+ * own seeded generator), which keeps a perturbation reproducible from the
+ * field alone.  To perturb K and V once for both ICL calls (the paper's
+ * "coordinated" setting), perturb them once and pass the results to the
+ * attention entry points; the test call then reads the same perturbed K/V.
+ *
+ *   x_dtype, z_dtype  TFM_F32 or TFM_BF16 (out has the type of x)
+ *   x, z              (B, S, H, D) device inputs
+ *   eps               the perturbation strength, finite and >= 0
+ *   out               (B, S, H, D) device output; may be x itself (in place)
+ *                     or z itself, but must not partially overlap either
+ *   rho               (B, H) float32 device output, or NULL
+ *   workspace         >= tfm_noise_per_head_workspace_bytes(B, H, S, D) bytes
+ *
+ * D must be a multiple of 8 (TFM_ERR_UNSUPPORTED_HEAD_DIM otherwise);
+ * H*D <= 16384, B*H <= 65535 and B*S*H*D <= 2^40 (TFM_ERR_BAD_SHAPE).
+ * S == 0 is valid: nothing is read or written except rho, which is set to 0;
+ * x, z, out and workspace may then be NULL.  Pointers 16-byte aligned.
+ */
+size_t tfm_noise_per_head_workspace_bytes(int B, int H, int S, int D);
+int tfm_noise_per_head(int x_dtype, int z_dtype, int B, int H, int S, int D, const void* x,
+                       const void* z, float eps, void* out, float* rho, void* workspace,
+                       size_t workspace_bytes, tfm_stream stream);
 
 #ifdef __cplusplus
 }

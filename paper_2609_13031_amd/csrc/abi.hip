@@ -113,15 +113,16 @@ const char* tfm_status_string(int status) {
   switch (status) {
     case TFM_OK: return "TFM_OK";
     case TFM_ERR_NULL_PTR: return "TFM_ERR_NULL_PTR: a required pointer is NULL";
-    case TFM_ERR_BAD_SHAPE: return "TFM_ERR_BAD_SHAPE: B, H >= 1, N >= 1, M >= 0 and sizes within limits required";
+    case TFM_ERR_BAD_SHAPE: return "TFM_ERR_BAD_SHAPE: B, H >= 1, N >= 1, M >= 0 (S >= 0) and sizes within limits required";
     case TFM_ERR_BAD_DTYPE: return "TFM_ERR_BAD_DTYPE: unsupported dtype code";
-    case TFM_ERR_UNSUPPORTED_HEAD_DIM: return "TFM_ERR_UNSUPPORTED_HEAD_DIM: D must be 64 or 128";
+    case TFM_ERR_UNSUPPORTED_HEAD_DIM:
+      return "TFM_ERR_UNSUPPORTED_HEAD_DIM: D must be 64 or 128 (a multiple of 8 for the noise operator)";
     case TFM_ERR_MISALIGNED: return "TFM_ERR_MISALIGNED: pointers must be 16-byte aligned";
     case TFM_ERR_WORKSPACE_TOO_SMALL: return "TFM_ERR_WORKSPACE_TOO_SMALL: workspace below the size query";
     case TFM_ERR_HIP: return "TFM_ERR_HIP: the HIP runtime reported an error";
     case TFM_ERR_BAD_ARG:
-      return "TFM_ERR_BAD_ARG: alpha must be finite and positive, q_scale_mode one of TFM_QSCALE_*, "
-             "test_kv_heads 0 or a divisor of H";
+      return "TFM_ERR_BAD_ARG: alpha must be finite and positive, eps finite and >= 0, q_scale_mode one of "
+             "TFM_QSCALE_*, test_kv_heads 0 or a divisor of H";
     default: return "TFM_ERR_UNKNOWN";
   }
 }
@@ -287,6 +288,47 @@ int tfm_icl_attention(int in_dtype, int out_dtype, const tfm_icl_options* opts, 
                                 o_test, stream);
   if (st == TFM_OK && used_fp8) *used_fp8 = fp8 ? 1 : 0;
   return st;
+}
+
+// ---- Eq. (3) noise operator ----
+
+static int check_noise_shape(int B, int H, int S, int D) {
+  if (B < 1 || H < 1 || S < 0) return TFM_ERR_BAD_SHAPE;
+  if (D < 8 || D % 8 != 0) return TFM_ERR_UNSUPPORTED_HEAD_DIM;
+  if ((long long)B * H > 65535 || (long long)H * D > 16384) return TFM_ERR_BAD_SHAPE;
+  if ((long double)B * S * H * D > 1099511627776.0L) return TFM_ERR_BAD_SHAPE;  // 2^40 elements
+  return TFM_OK;
+}
+
+static size_t noise_partial_bytes(int B, int H, int S, int D) {
+  const int rpc = noise_rows_per_chunk(H, D);
+  const size_t chunks = ((size_t)S + rpc - 1) / rpc;
+  return align256(chunks * B * H * sizeof(double));
+}
+
+size_t tfm_noise_per_head_workspace_bytes(int B, int H, int S, int D) {
+  if (check_noise_shape(B, H, S, D) != TFM_OK) return 0;
+  return noise_partial_bytes(B, H, S, D) + align256((size_t)B * H * sizeof(float));
+}
+
+int tfm_noise_per_head(int x_dtype, int z_dtype, int B, int H, int S, int D, const void* x, const void* z, float eps,
+                       void* out, float* rho, void* workspace, size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_noise_shape(B, H, S, D));
+  if ((x_dtype != TFM_F32 && x_dtype != TFM_BF16) || (z_dtype != TFM_F32 && z_dtype != TFM_BF16))
+    return TFM_ERR_BAD_DTYPE;
+  if (!std::isfinite(eps) || eps < 0.0f) return TFM_ERR_BAD_ARG;
+  if (rho && !aligned16(rho)) return TFM_ERR_MISALIGNED;
+  hipStream_t s = (hipStream_t)stream;
+  if (S == 0) {  // nothing to perturb; rho of an empty head is 0
+    if (rho) TFM_HIP(launch_fill_zero_u32((uint32_t*)rho, B * H, s));
+    return TFM_OK;
+  }
+  const void* req[] = {x, z, out, workspace};
+  TFM_TRY(check_io(false, req, 4, nullptr, 0));
+  if (workspace_bytes < tfm_noise_per_head_workspace_bytes(B, H, S, D)) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* ws = (uint8_t*)workspace;
+  return hip_status(launch_noise(x_dtype == TFM_BF16, z_dtype == TFM_BF16, B, H, S, D, x, z, eps, out,
+                                 (double*)ws, (float*)(ws + noise_partial_bytes(B, H, S, D)), rho, s));
 }
 
 }  // extern "C"

@@ -15,7 +15,7 @@ PKG = os.path.dirname(HERE)
 ROOT = os.path.dirname(PKG)
 OUT = os.path.join(PKG, "libtfm.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
-SOURCES = ["abi.hip", "quantize.hip", "attn_fp8.hip", "attn_bf16.hip"]
+SOURCES = ["abi.hip", "quantize.hip", "attn_fp8.hip", "attn_bf16.hip", "noise.hip"]
 
 FLAGS = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", "-Wall",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -70,4 +70,11 @@ hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N
                             const void* q_train, const void* q_test, const void* k,
                             const void* v, void* o_train, void* o_test, hipStream_t s);
 
+// Eq. (3) perturbation: sum of squares per (row chunk, b, h) into partial
+// (chunks*B*H doubles), rho (B*H floats, also copied to rho_out when non-NULL),
+// then out = x + fl32(eps*rho)*z.  Requires S >= 1, D % 8 == 0, H*D <= 16384.
+int noise_rows_per_chunk(int H, int D);
+hipError_t launch_noise(int x_bf16, int z_bf16, int B, int H, int S, int D, const void* x, const void* z, float eps,
+                        void* out, double* partial, float* rho, float* rho_out, hipStream_t s);
+
 }  // namespace tfm

@@ -54,6 +54,8 @@ SIGNATURES = {
     "tfm_icl_attention_workspace_bytes": (_c_size, [_c_int] * 6),
     "tfm_icl_attention": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6
                           + [_c_int, ctypes.POINTER(_c_int), _p, _c_size, _p]),
+    "tfm_noise_per_head_workspace_bytes": (_c_size, [_c_int] * 4),
+    "tfm_noise_per_head": (_c_int, [_c_int] * 6 + [_p, _p, _c_float, _p, _p, _p, _c_size, _p]),
 }
 
 
@@ -303,3 +305,30 @@ def tfm_icl_attention(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.fl
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None),
           int(fp8_min_train_rows), ctypes.byref(used), _ptr(ws), 0 if ws is None else ws.numel(), _stream())
     return o_tr, o_te, bool(used.value)
+
+
+def tfm_noise_per_head_workspace_bytes(B, H, S, D):
+    return lib().tfm_noise_per_head_workspace_bytes(B, H, S, D)
+
+
+def tfm_noise_per_head(x, z, eps, out=None, workspace=None):
+    """Eq. (3): x + eps * rho * z per (table, head), rho the head's RMS; returns (out, rho (B,H) fp32).
+
+    x and z are (B, S, H, D) float32 or bfloat16 (z may differ from x); out has the type of x
+    and may be x itself (in place)."""
+    B, S, H, D = _shape_bnhd(x, "x")
+    if tuple(z.shape) != (B, S, H, D):
+        raise ValueError("z must have the shape of x")
+    if x.dtype not in _DTYPES or z.dtype not in _DTYPES:
+        raise ValueError("x and z must be float32 or bfloat16")
+    dev = _check_inputs({"x": x, "z": z})
+    if out is None:
+        out = torch.empty_like(x)
+    elif tuple(out.shape) != (B, S, H, D) or out.dtype != x.dtype or not out.is_contiguous():
+        raise ValueError("out must be a contiguous tensor of the shape and type of x")
+    rho = torch.empty((B, H), dtype=torch.float32, device=dev)
+    nws = tfm_noise_per_head_workspace_bytes(B, H, S, D)
+    ws = workspace if workspace is not None else torch.empty(max(nws, 1), dtype=torch.uint8, device=dev)
+    _call("tfm_noise_per_head", _DTYPES[x.dtype], _DTYPES[z.dtype], B, H, S, D, _ptr(x), _ptr(z), float(eps),
+          _ptr(out), _ptr(rho), _ptr(ws), ws.numel(), _stream())
+    return out, rho

@@ -20,7 +20,7 @@ def header_functions():
 def test_library_exports_every_declared_function():
     L = tfm.lib()
     names = header_functions()
-    assert len(names) == 14
+    assert len(names) == 16
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(tfm.SIGNATURES)
@@ -136,3 +136,23 @@ def test_gate_selects_the_path_before_validating_it():
     assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 8193, 3, -1) == tfm.tfm_icl_attention_fp8_workspace_bytes(
         1, 2, 64, 8193, 3)
     assert L.tfm_icl_attention_workspace_bytes(1, 2, 64, 100, 3, 99) > 0
+
+
+def test_noise_validation_and_workspace():
+    L = tfm.lib()
+    n = lambda **kw: L.tfm_noise_per_head(kw.get("xd", 1), kw.get("zd", 0), kw.get("B", 2), kw.get("H", 3),
+                                          kw.get("S", 100), kw.get("D", 64), kw.get("x", FAKE), kw.get("z", FAKE),
+                                          kw.get("eps", 0.1), kw.get("out", FAKE), kw.get("rho"), kw.get("ws", FAKE),
+                                          kw.get("nws", 8), None)
+    # every call here fails validation (the workspace is always too small when nothing else is wrong)
+    assert n() == 6
+    assert n(B=0) == 2 and n(H=0) == 2 and n(S=-1) == 2 and n(H=300, D=64) == 2 and n(B=70000, H=1) == 2
+    assert n(D=12) == 4 and n(D=0) == 4 and n(D=4) == 4
+    assert n(xd=2) == 3 and n(zd=5) == 3
+    assert n(eps=-0.5) == 8 and n(eps=float("nan")) == 8 and n(eps=float("inf")) == 8
+    assert n(x=None) == 1 and n(z=None) == 1 and n(out=None) == 1 and n(ws=None) == 1
+    assert n(x=MIS) == 5 and n(out=MIS) == 5 and n(rho=MIS) == 5 and n(rho=MIS, S=0) == 5
+    ws = tfm.tfm_noise_per_head_workspace_bytes
+    # fixed-order partial sums: one double per (row chunk, b, h), chunks of ceil(32768 / (H D)) rows, then rho
+    assert ws(2, 6, 65536, 64) == ((65536 + 85) // 86 * 12 * 8 + 255) // 256 * 256 + 256
+    assert ws(1, 1, 1, 8) == 512 and ws(1, 1, 0, 8) == 256 and ws(1, 1, 5, 12) == 0
