@@ -26,21 +26,22 @@ if ROOT not in sys.path:
 METRIC = "FP8 ICL attention TFLOP/s + speedup vs bf16 at N_train=65536, 1 MI355X"
 FP8_PEAK_TFLOPS = 5000.0          # MI355X dense FP8 MFMA
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
-ATTN_SRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc", "attn_fp8.hip")
+CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
+HBM_PEAK_GBS = 8000.0
 
 
 def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
-def source_digest():
-    with open(ATTN_SRC, "rb") as f:
+def source_digest(name):
+    with open(os.path.join(CSRC, name), "rb") as f:
         return hashlib.sha256(f.read()).hexdigest()[:16]
 
 
-def traffic_from_counters(n_dispatch_units):
-    """HBM bytes per attention launch from the committed rocprofv3 --pmc summary,
-    or None when it is missing or was taken on a different attn_fp8.hip."""
+def counter_value(key, source):
+    """A figure from the committed rocprofv3 --pmc summary, or None when it is missing
+    or was taken on a different version of the kernel source it measures."""
     if not os.path.exists(COUNTERS):
         return None
     kv = {}
@@ -48,16 +49,24 @@ def traffic_from_counters(n_dispatch_units):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
-    if kv.get("attn_fp8_source_sha256_16") != source_digest():
+    if kv.get(source.replace(".hip", "") + "_source_sha256_16") != source_digest(source):
         return None
     try:
-        return float(kv["hbm_bytes_per_launch"])
+        return float(kv[key])
     except (KeyError, ValueError):
         return None
 
 
-def cpu_baseline(x, w, rows):
-    """The oracle, single-threaded, on a bounded sample of the same workload."""
+def metrics(got, ref):
+    import numpy as np
+    d = np.abs(np.asarray(got, np.float64) - ref)
+    rms = float(np.sqrt(np.mean(ref ** 2)))
+    return {"relF": float(np.linalg.norm(d) / np.linalg.norm(ref)), "max_abs_over_rms": float(d.max() / rms)}
+
+
+def cpu_baseline(x, w, rows, block_kv):
+    """The oracle, single-threaded, on a bounded sample of the same workload; also returns
+    its quantized codes and its O_qp rows (table 0, head 0) for the accuracy report."""
     import numpy as np
     from threadpoolctl import threadpool_limits
     from oracle import attention as OA
@@ -69,14 +78,34 @@ def cpu_baseline(x, w, rows):
         qz = OQ.quantize_qkv_per_head(sl(x["q_train"]), sl(x["k"]), sl(x["v"]), sl(x["q_test"]))
         t_quant = time.perf_counter() - t0
         t0 = time.perf_counter()
-        OA.icl_attention_fp8_kernel_model(qz, w.alpha, 64, np.arange(rows), [])
+        o_qp, _ = OA.icl_attention_fp8_kernel_model(qz, w.alpha, block_kv, np.arange(rows), [])
         t_attn = time.perf_counter() - t0
     flops = 4.0 * w.D * w.N * rows
     return {"value": flops / t_attn / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
             "sample": "one-pass FP8 kernel model (fp64 numpy) for %d train query rows of table 0, head 0, "
                       "against all %d keys; quantization of that head (N+M rows) took %.2f s more" %
                       (rows, w.N, t_quant),
-            "seconds": round(t_attn, 2)}
+            "seconds": round(t_attn, 2)}, o_qp[0, :, 0]
+
+
+def accuracy(x, w, o_qp, gpu_fp8, gpu_bf16, rows):
+    """Errors on train rows [0, rows) of table 0, head 0: the FP8 kernel against the oracle's
+    kernel model (O_qp) and against unquantized fp64 attention (O_exact), the method's own
+    quantization error (O_qp against O_exact) and the bf16 kernel against O_exact."""
+    import numpy as np
+    from oracle import attention as OA
+
+    q = x["q_train"][0, :rows, 0].astype(np.float64)
+    exact = OA.softmax_attention(q, x["k"][0, :, 0].astype(np.float64), x["v"][0, :, 0].astype(np.float64),
+                                 float(w.alpha))
+    qp = o_qp[:rows]
+    out = {"rows": "train rows 0..%d of table 0, head 0 (fp32 outputs)" % (rows - 1),
+           "fp8_kernel_vs_kernel_model": metrics(gpu_fp8, qp),
+           "fp8_kernel_vs_fp64_exact": metrics(gpu_fp8, exact),
+           "kernel_model_vs_fp64_exact": metrics(qp, exact)}
+    if gpu_bf16 is not None:
+        out["bf16_kernel_vs_fp64_exact"] = metrics(gpu_bf16, exact)
+    return out
 
 
 def time_sdpa(g, w, steps, warmup):
@@ -192,6 +221,8 @@ def main():
     ap.add_argument("--workload", default="mid")
     ap.add_argument("--cpu-rows", type=int, default=8192, help="query rows of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--accuracy-rows", type=int, default=1024,
+                    help="rows of the oracle sample also compared with fp64 attention (with the CPU baseline)")
     ap.add_argument("--no-bf16", action="store_true")
     ap.add_argument("--sdpa", action="store_true",
                     help="also time torch's scaled_dot_product_attention (flash backend, bf16) as context")
@@ -305,7 +336,11 @@ def main():
 
     value = w.flops / ms_step / 1e9                      # TFLOP/s
     achieved = w.flops / attn_ms / 1e9
-    traffic = traffic_from_counters(1)
+    traffic = counter_value("hbm_bytes_per_launch", "attn_fp8.hip")
+    in_bytes = 4 if w.dtype == "f32" else 2
+    q_elems = (3 * w.N + w.M) * w.B * w.H * w.D
+    q_algo = q_elems * (in_bytes + 1)                    # inputs read once, e4m3 codes written
+    q_gbs = q_algo / quant_ms / 1e6
     result = {
         "metric": METRIC, "value": round(value, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": K,
         "warmup": args.warmup, "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
@@ -322,10 +357,27 @@ def main():
         "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": traffic},
+        "quantize_hbm": {"stage": "amax + scales + codes of Q_train, K, V, Q_test (5 launches)",
+                         "ms": round(quant_ms, 4), "algorithmic_bytes": q_algo, "achieved": round(q_gbs, 1),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(q_gbs / HBM_PEAK_GBS, 4),
+                         "traffic": counter_value("quantize_stage_hbm_bytes_per_step", "quantize.hip")},
     }
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) on %d rows" % args.cpu_rows)
-        result["cpu_baseline"] = cpu_baseline(x, w, args.cpu_rows)
+        bkv = tfm.tfm_icl_attention_fp8_block_kv(w.D)
+        result["cpu_baseline"], o_qp = cpu_baseline(x, w, args.cpu_rows, bkv)
+        # one more FP8 call (and bf16 call) with fp32 outputs, outside the timed region
+        f_tr, f_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha,
+                                               workspace=ws)
+        r = min(args.accuracy_rows, args.cpu_rows)
+        gpu_fp8 = f_tr[0, :r, 0].cpu().numpy()
+        gpu_bf16 = None
+        if not args.no_bf16:
+            gpu_bf16 = tfm.tfm_icl_attention_bf16(gb["q_train"][:1], gb["k"][:1], gb["v"][:1], None,
+                                                  alpha=w.alpha)[0][0, :r, 0].cpu().numpy()
+        del f_tr, f_te
+        log("accuracy on %d rows" % r)
+        result["accuracy"] = accuracy(x, w, o_qp, gpu_fp8, gpu_bf16, r)
     print(json.dumps(result), flush=True)
 
 

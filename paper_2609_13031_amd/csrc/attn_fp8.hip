@@ -200,39 +200,46 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
     const float bias = 8.0f - c * m_new;                                   // lifts the running max to 2^8
     m_run = m_new;
 
-    // ---- P~ = 2^(c S + bias) rounded to e4m3, directly the B operand of the PV product ----
-    v8i pf[NP];
-#pragma unroll
-    for (int p = 0; p < NP; ++p)
-#pragma unroll
-      for (int w = 0; w < 8; ++w) {
-        const v16f& src = st[2 * p + w / 4];
-        const int r = 4 * (w % 4);
-        pf[p][w] = pack4_e4m3(__builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 0], c, bias)),
-                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 1], c, bias)),
-                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 2], c, bias)),
-                              __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 3], c, bias)));
-      }
+    // Exact skip: when every row's largest exponent in this block is <= -11, every
+    // lifted weight 2^(c s + bias) < 2^-10 (with v_exp_f32's sub-ulp error) rounds
+    // to e4m3 zero, and the running max did not move (the row max alone would
+    // give exponent 8), so the block changes neither l nor O.
+    if (__builtin_amdgcn_ballot_w64(__builtin_fmaf(mx, c, bias) > -11.0f)) {
 
-    // ---- l += sum P_8 (row-sum MFMA) and O^T += V_8^T P_8^T ----
-    // Rescale the running state only when some row's max grew (rescale is exactly
-    // 1 where it did not).  Written element-wise so the accumulators are scaled in
-    // place inside the wave-uniform branch.
-    if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
+      // ---- P~ = 2^(c S + bias) rounded to e4m3, directly the B operand of the PV product ----
+      v8i pf[NP];
 #pragma unroll
-      for (int i = 0; i < D / 32; ++i)
+      for (int p = 0; p < NP; ++p)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) acc_o[i][j] = acc_o[i][j] * rescale;
+        for (int w = 0; w < 8; ++w) {
+          const v16f& src = st[2 * p + w / 4];
+          const int r = 4 * (w % 4);
+          pf[p][w] = pack4_e4m3(__builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 0], c, bias)),
+                                __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 1], c, bias)),
+                                __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 2], c, bias)),
+                                __builtin_amdgcn_exp2f(__builtin_fmaf(src[r + 3], c, bias)));
+        }
+
+      // ---- l += sum P_8 (row-sum MFMA) and O^T += V_8^T P_8^T ----
+      // Rescale the running state only when some row's max grew (rescale is exactly
+      // 1 where it did not).  Written element-wise so the accumulators are scaled in
+      // place inside the wave-uniform branch.
+      if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) lacc[j] = lacc[j] * rescale;
-    }
+        for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-    for (int p = 0; p < NP; ++p) {
-      lacc = mfma_f8_16x16x128(ones, pf[p], lacc);
+          for (int j = 0; j < 16; ++j) acc_o[i][j] = acc_o[i][j] * rescale;
 #pragma unroll
-      for (int i = 0; i < D / 32; ++i)
-        acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (p * D + 32 * i + ql) * VS + 32 * half), pf[p], acc_o[i]);
-    }
+        for (int j = 0; j < 4; ++j) lacc[j] = lacc[j] * rescale;
+      }
+#pragma unroll
+      for (int p = 0; p < NP; ++p) {
+        lacc = mfma_f8_16x16x128(ones, pf[p], lacc);
+#pragma unroll
+        for (int i = 0; i < D / 32; ++i)
+          acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (p * D + 32 * i + ql) * VS + 32 * half), pf[p], acc_o[i]);
+      }
+    }  // not skipped
 
     if (more) {
       uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
