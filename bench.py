@@ -28,6 +28,11 @@ FP8_PEAK_TFLOPS = 5000.0          # MI355X dense FP8 MFMA
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
 CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
 HBM_PEAK_GBS = 8000.0
+# The FP8 kernel's VALU work per (query, key) score is one v_fma_f32, one v_exp_f32, half a
+# v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (3.29, 8.66, 8.84 and
+# 5.67 cycles per wave64 instruction) over 1024 SIMDs at 2.4 GHz give this many scores per
+# second at most, i.e. 4*D times it in FLOP/s.
+ALU_SCORES_PER_S = 1024 * 2.4e9 * 64 / (3.29 + 8.66 + 8.84 / 2 + 5.67 / 2)
 
 
 def log(*a):
@@ -357,6 +362,10 @@ def main():
         "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
                      "traffic": traffic},
+        "alu_roofline": {"kernel": "attn_fp8_kernel", "bound": "alu", "achieved": round(achieved, 2),
+                         "peak": round(ALU_SCORES_PER_S * 4 * w.D / 1e12, 1), "unit": "TFLOP/s",
+                         "frac": round(achieved / (ALU_SCORES_PER_S * 4 * w.D / 1e12), 4),
+                         "note": "VALU issue ceiling of the softmax work per score (exp, fma, e4m3 convert, max)"},
         "quantize_hbm": {"stage": "amax + scales + codes of Q_train, K, V, Q_test (5 launches)",
                          "ms": round(quant_ms, 4), "algorithmic_bytes": q_algo, "achieved": round(q_gbs, 1),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(q_gbs / HBM_PEAK_GBS, 4),

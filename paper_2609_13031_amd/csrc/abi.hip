@@ -97,11 +97,13 @@ int quantize_all(int in_dtype, int q_scale_mode, int B, int H, int D, int N, int
   TFM_HIP(launch_fill_zero_u32(amax, 4 * BH, s));
   TFM_HIP(launch_amax(bf, B, H, D, N, M, q_train, k, v, test_amax ? q_test : nullptr, amax, s));
   TFM_HIP(launch_scales(BH, q_scale_mode, amax, scales, s_q, s_k, s_v, s_q_test, s));
-  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, q_train, scales, q8_train, s));
-  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, q8_test, s));
-  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, k, scales + BH, k8, s));
+  // V, K, then the queries: the reverse of the order the amax pass read them in, so the
+  // second read of the most recently scanned tensors can still hit the memory-side cache
   if (v8) TFM_HIP(launch_quantize_rows(bf, B, H, D, N, v, scales + 2 * BH, v8, s));
   else TFM_HIP(launch_quantize_v_tiles(bf, B, H, D, N, v, scales + 2 * BH, v8t, s));
+  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, k, scales + BH, k8, s));
+  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, q_train, scales, q8_train, s));
+  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, q8_test, s));
   return TFM_OK;
 }
 

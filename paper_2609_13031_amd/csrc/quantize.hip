@@ -99,8 +99,20 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(int B, int H, int D, int
     for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
       uint32_t m = 0;
       const T* base = x + ((size_t)b * N) * H * D + (size_t)p * VEC;
-      for (int row = r0 + rr; row < r1; row += rm.rows_per_iter) {
-        u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)row * H * D);
+      const size_t step = (size_t)rm.rows_per_iter * H * D;
+      int row = r0 + rr;
+      // four independent 16-byte loads in flight per thread, then the remainder
+      for (; row + 3 * rm.rows_per_iter < r1; row += 4 * rm.rows_per_iter) {
+        const T* src = base + (size_t)row * H * D;
+        const u32x4 w0 = *reinterpret_cast<const u32x4*>(src);
+        const u32x4 w1 = *reinterpret_cast<const u32x4*>(src + step);
+        const u32x4 w2 = *reinterpret_cast<const u32x4*>(src + 2 * step);
+        const u32x4 w3 = *reinterpret_cast<const u32x4*>(src + 3 * step);
+        m = max(max(m, absmax_bits(w0, (T*)nullptr)), absmax_bits(w1, (T*)nullptr));
+        m = max(max(m, absmax_bits(w2, (T*)nullptr)), absmax_bits(w3, (T*)nullptr));
+      }
+      for (; row < r1; row += rm.rows_per_iter) {
+        const u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)row * H * D);
         m = max(m, absmax_bits(w, (T*)nullptr));
       }
       atomicMax(&smax[p * VEC / D], m);
@@ -145,9 +157,9 @@ __global__ __launch_bounds__(kThreads) void quantize_rows_kernel(int H, int D, i
                                                                  uint8_t* __restrict__ codes) {
   constexpr int VEC = Vec<T>::n;
   const int b = blockIdx.y;
+  const int r0 = blockIdx.x * rows_per_chunk;
   const RowMap rm(H, D, VEC);
   const int t = threadIdx.x;
-  const int r0 = blockIdx.x * rows_per_chunk;
   const int r1 = min(rows, r0 + rows_per_chunk);
   if (t >= rm.rows_per_iter * rm.lanes_per_row) return;
   const int rr = t / rm.lanes_per_row;
@@ -156,17 +168,30 @@ __global__ __launch_bounds__(kThreads) void quantize_rows_kernel(int H, int D, i
     const float s = scale[b * H + h];
     const T* src = x + ((size_t)b * rows) * H * D + (size_t)p * VEC;
     uint8_t* dst = codes + (((size_t)b * H + h) * rows) * D + d0;
-    for (int row = r0 + rr; row < r1; row += rm.rows_per_iter) {
-      u32x4 w = *reinterpret_cast<const u32x4*>(src + (size_t)row * H * D);
-      float xv[VEC];
-      unpack(w, xv, (T*)nullptr);
-      if constexpr (VEC == 4) {
-        *reinterpret_cast<uint32_t*>(dst + (size_t)row * D) = codes4(xv, s);
-      } else {
-        uint2 o;
-        o.x = codes4(xv, s);
-        o.y = codes4(xv + 4, s);
-        *reinterpret_cast<uint2*>(dst + (size_t)row * D) = o;
+    // U rows per thread-iteration: their loads are all issued before any is converted
+    constexpr int U = 4;
+    int row = r0 + rr;
+    for (; row < r1; row += U * rm.rows_per_iter) {
+      u32x4 w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ru = row + u * rm.rows_per_iter;
+        w[u] = ru < r1 ? *reinterpret_cast<const u32x4*>(src + (size_t)ru * H * D) : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int ru = row + u * rm.rows_per_iter;
+        if (ru >= r1) break;
+        float xv[VEC];
+        unpack(w[u], xv, (T*)nullptr);
+        if constexpr (VEC == 4) {
+          *reinterpret_cast<uint32_t*>(dst + (size_t)ru * D) = codes4(xv, s);
+        } else {
+          uint2 o;
+          o.x = codes4(xv, s);
+          o.y = codes4(xv + 4, s);
+          *reinterpret_cast<uint2*>(dst + (size_t)ru * D) = o;
+        }
       }
     }
   }
@@ -209,22 +234,32 @@ __global__ __launch_bounds__(kThreads) void v_tiles_kernel(int H, int D, int N, 
     constexpr int VEC = Vec<T>::n;
     const float s = scale[bh];
     const int per_row = D / VEC;
-    for (int i = threadIdx.x; i < 64 * per_row; i += kThreads) {
-      const int kk = i / per_row, c = i % per_row;
-      const int key = kt * 64 + kk;
-      uint32_t cw[VEC / 4];
+    const int items = 64 * per_row;       // a multiple of 2 * 256 for D = 64 and 128
+    constexpr int U = 2;
+    for (int i0 = threadIdx.x; i0 < items; i0 += U * kThreads) {
+      u32x4 w[U];
 #pragma unroll
-      for (int j = 0; j < VEC / 4; ++j) cw[j] = 0u;
-      if (key < N) {
-        u32x4 w = *reinterpret_cast<const u32x4*>(src + (((size_t)b * N + key) * H + h) * D + c * VEC);
-        float xv[VEC];
-        unpack(w, xv, (T*)nullptr);
-#pragma unroll
-        for (int j = 0; j < VEC / 4; ++j) cw[j] = codes4(xv + 4 * j, s);
+      for (int u = 0; u < U; ++u) {       // loads first
+        const int i = i0 + u * kThreads;
+        const int key = kt * 64 + i / per_row;
+        w[u] = (i < items && key < N)
+                   ? *reinterpret_cast<const u32x4*>(src + (((size_t)b * N + key) * H + h) * D + (i % per_row) * VEC)
+                   : u32x4{0u, 0u, 0u, 0u};
       }
-      const int pos = v_tile_pos(kk);
 #pragma unroll
-      for (int j = 0; j < VEC; ++j) tile_codes[(c * VEC + j) * 64 + pos] = (uint8_t)(cw[j / 4] >> (8 * (j % 4)));
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * kThreads;
+        if (i >= items) break;
+        const int kk = i / per_row, c = i % per_row;
+        uint32_t cw[VEC / 4];
+        float xv[VEC];
+        unpack(w[u], xv, (T*)nullptr);
+#pragma unroll
+        for (int j = 0; j < VEC / 4; ++j) cw[j] = codes4(xv + 4 * j, s);   // zero inputs give code 0
+        const int pos = v_tile_pos(kk);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) tile_codes[(c * VEC + j) * 64 + pos] = (uint8_t)(cw[j / 4] >> (8 * (j % 4)));
+      }
     }
   }
   __syncthreads();
@@ -234,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void v_tiles_kernel(int H, int D, int N, 
 }
 
 int chunk_rows(int rows, int H, int D, int esize) {
-  // about 64 KiB of input per block
+  // about 64 KiB of input per block (measured best among 64 KiB .. 512 KiB)
   long per_row = (long)H * D * esize;
   long r = (65536 + per_row - 1) / per_row;
   if (r < 1) r = 1;
