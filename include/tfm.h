@@ -180,6 +180,41 @@ int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int
                                  size_t workspace_bytes, tfm_stream stream);
 
 /*
+ * tfm_icl_attention_fp8_fit / tfm_icl_attention_fp8_predict -- the two ICL
+ * calls split the way a tabular foundation model is used: fit once on the
+ * train rows, then predict any number of test batches against the same
+ * quantized keys and values.  With the train-query scale shared by the test
+ * queries (Sec. 3, the paragraph after Eq. (2)) a test row's output does not
+ * depend on its batch, so the train-side state can be kept.
+ *
+ * fit: Eq. (2) for Q_train, K and V, then the train-train call into o_train.
+ *   The workspace keeps the quantized train state (scales, Q_train, K, V
+ *   codes) for later predict calls; size it with
+ *   tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M_max) for the largest
+ *   test batch M_max to come (M_max = 0 if none).
+ * predict: Q_test (B, M, H, D) quantized with the train-query scale (or, with
+ *   TFM_QSCALE_PER_CALL, its own per-head scale), then the test-train call into
+ *   o_test (B, M, H, D), against the state of the last fit on this workspace.
+ *   workspace_bytes must be >= tfm_icl_attention_fp8_workspace_bytes(B, H, D,
+ *   N, M); B, H, D, N must be those of the fit.  M == 0 does nothing.
+ *
+ * Both produce, bit for bit, the rows tfm_icl_attention_fp8 returns for the
+ * same inputs.  TFM_QSCALE_JOINT needs the test rows at fit time and is
+ * rejected (TFM_ERR_BAD_ARG); opts->test_kv_heads applies to predict.  Calls
+ * on one workspace must be ordered (one stream, or synchronized); a predict
+ * overwrites the test part of the workspace only, so predicts on different
+ * streams need different workspaces holding the same fit state.
+ */
+int tfm_icl_attention_fp8_fit(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H,
+                              int D, int N, float alpha, const void* q_train, const void* k,
+                              const void* v, void* o_train, void* workspace,
+                              size_t workspace_bytes, tfm_stream stream);
+int tfm_icl_attention_fp8_predict(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B,
+                                  int H, int D, int N, int M, float alpha, const void* q_test,
+                                  void* o_test, void* workspace, size_t workspace_bytes,
+                                  tfm_stream stream);
+
+/*
  * tfm_icl_attention_fp8_prequantized -- the attention part of
  * tfm_icl_attention_fp8 on codes and scales produced by
  * tfm_quantize_qkv_per_head (same layouts), e.g. to reuse K_8 / V_8 for

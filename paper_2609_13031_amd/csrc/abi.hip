@@ -21,9 +21,9 @@ Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M) {
   w.amax = off;      off += align256(4 * bh * sizeof(uint32_t));
   w.scales = off;    off += align256(4 * bh * sizeof(float));
   w.q8_train = off;  off += align256(bh * N * D);
-  w.q8_test = off;   off += align256(bh * (size_t)M * D);
   w.k8 = off;        off += align256(bh * N * D);
   w.v8t = off;       off += align256(v8t_bytes(B, H, D, N));
+  w.q8_test = off;   off += align256(bh * (size_t)M * D);
   w.total = off;
   return w;
 }
@@ -95,7 +95,7 @@ int quantize_all(int in_dtype, int q_scale_mode, int B, int H, int D, int N, int
   const int BH = B * H;
   const bool test_amax = q_scale_mode != TFM_QSCALE_SHARED && M > 0;
   TFM_HIP(launch_fill_zero_u32(amax, 4 * BH, s));
-  TFM_HIP(launch_amax(bf, B, H, D, N, M, q_train, k, v, test_amax ? q_test : nullptr, amax, s));
+  TFM_HIP(launch_amax(bf, 0, test_amax ? 3 : 2, B, H, D, N, M, q_train, k, v, q_test, amax, s));
   TFM_HIP(launch_scales(BH, q_scale_mode, amax, scales, s_q, s_k, s_v, s_q_test, s));
   // V, K, then the queries: the reverse of the order the amax pass read them in, so the
   // second read of the most recently scanned tensors can still hit the memory-side cache
@@ -196,7 +196,8 @@ int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int
   const uint8_t* ws = (const uint8_t*)workspace;
   const float* scales = (const float*)(ws + L.scales);
   const int BH = B * H;
-  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, o.test_kv_heads, alpha, ws + L.q8_train,
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTrain | kCallTest, B, H, D, N, M, o.test_kv_heads,
+                                    alpha, ws + L.q8_train,
                                     ws + L.q8_test, ws + L.k8, ws + L.v8t, scales, scales + BH, scales + 2 * BH,
                                     scales + 3 * BH, o_train, o_test, (hipStream_t)stream));
 }
@@ -218,6 +219,66 @@ int tfm_icl_attention_fp8(int in_dtype, int out_dtype, const tfm_icl_options* op
                                          workspace_bytes, stream));
   return tfm_icl_attention_fp8_attend(out_dtype, opts, B, H, D, N, M, alpha, o_train, o_test, workspace,
                                       workspace_bytes, stream);
+}
+
+int tfm_icl_attention_fp8_fit(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N,
+                              float alpha, const void* q_train, const void* k, const void* v, void* o_train,
+                              void* workspace, size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, 0));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
+  if (o.q_scale_mode == TFM_QSCALE_JOINT) return TFM_ERR_BAD_ARG;   // needs the test rows at fit time
+  const void* req[] = {q_train, k, v, o_train, workspace};
+  TFM_TRY(check_io(false, req, 5, nullptr, 0));
+  const Fp8Workspace L = fp8_workspace_layout(B, H, D, N, 0);
+  if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  uint8_t* ws = (uint8_t*)workspace;
+  hipStream_t s = (hipStream_t)stream;
+  float* scales = (float*)(ws + L.scales);
+  const int BH = B * H;
+  TFM_TRY(quantize_all(in_dtype, TFM_QSCALE_SHARED, B, H, D, N, 0, q_train, k, v, nullptr, ws + L.q8_train,
+                       ws + L.k8, nullptr, ws + L.v8t, nullptr, (uint32_t*)(ws + L.amax), scales, nullptr, nullptr,
+                       nullptr, nullptr, s));
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTrain, B, H, D, N, 0, o.test_kv_heads, alpha,
+                                    ws + L.q8_train, nullptr, ws + L.k8, ws + L.v8t, scales, scales + BH,
+                                    scales + 2 * BH, scales + 3 * BH, o_train, nullptr, s));
+}
+
+int tfm_icl_attention_fp8_predict(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D,
+                                  int N, int M, float alpha, const void* q_test, void* o_test, void* workspace,
+                                  size_t workspace_bytes, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
+  if (o.q_scale_mode == TFM_QSCALE_JOINT) return TFM_ERR_BAD_ARG;
+  const void* req[] = {workspace};
+  const void* tst[] = {q_test, o_test};
+  TFM_TRY(check_io(M > 0, req, 1, tst, 2));
+  const Fp8Workspace L = fp8_workspace_layout(B, H, D, N, M);
+  if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  if (M == 0) return TFM_OK;
+  uint8_t* ws = (uint8_t*)workspace;
+  hipStream_t s = (hipStream_t)stream;
+  uint32_t* amax = (uint32_t*)(ws + L.amax);
+  float* scales = (float*)(ws + L.scales);
+  const int bf = in_dtype == TFM_BF16;
+  const int BH = B * H;
+  if (o.q_scale_mode == TFM_QSCALE_PER_CALL) {
+    TFM_HIP(launch_fill_zero_u32(amax + 3 * BH, BH, s));
+    TFM_HIP(launch_amax(bf, 3, 3, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, amax, s));
+  }
+  // the train slots of amax are the fit's, so s_q, s_k and s_v come out as they did then
+  TFM_HIP(launch_scales(BH, o.q_scale_mode, amax, scales, nullptr, nullptr, nullptr, nullptr, s));
+  TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, ws + L.q8_test, s));
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTest, B, H, D, N, M, o.test_kv_heads, alpha,
+                                    ws + L.q8_train, ws + L.q8_test, ws + L.k8, ws + L.v8t, scales, scales + BH,
+                                    scales + 2 * BH, scales + 3 * BH, nullptr, o_test, s));
 }
 
 size_t tfm_icl_attention_fp8_prequantized_workspace_bytes(int B, int H, int D, int N) {
@@ -244,7 +305,8 @@ int tfm_icl_attention_fp8_prequantized(int out_dtype, const tfm_icl_options* opt
   hipStream_t s = (hipStream_t)stream;
   uint8_t* v8t = (uint8_t*)workspace;
   TFM_HIP(launch_relayout_v_tiles(B, H, D, N, v8, v8t, s));
-  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, B, H, D, N, M, o.test_kv_heads, alpha, q8_train, q8_test,
+  return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTrain | kCallTest, B, H, D, N, M, o.test_kv_heads,
+                                    alpha, q8_train, q8_test,
                                     k8, v8t, s_q, s_k, s_v, s_q_test ? s_q_test : s_q, o_train, o_test, s));
 }
 

@@ -273,14 +273,15 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
 
 }  // namespace
 
-hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads, float alpha,
-                           const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8, const uint8_t* v8t,
-                           const float* s_q, const float* s_k, const float* s_v, const float* s_q_test,
-                           void* o_train, void* o_test, hipStream_t s) {
+hipError_t launch_attn_fp8(int out_bf16, int calls, int B, int H, int D, int N, int M, int test_kv_heads,
+                           float alpha, const uint8_t* q8_train, const uint8_t* q8_test, const uint8_t* k8,
+                           const uint8_t* v8t, const float* s_q, const float* s_k, const float* s_v,
+                           const float* s_q_test, void* o_train, void* o_test, hipStream_t s) {
   Fp8Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
-  a.tiles_train = (N + kRowsPerBlock - 1) / kRowsPerBlock;
-  a.tiles = a.tiles_train + (M + kRowsPerBlock - 1) / kRowsPerBlock;
+  a.tiles_train = (calls & kCallTrain) ? (N + kRowsPerBlock - 1) / kRowsPerBlock : 0;
+  a.tiles = a.tiles_train + ((calls & kCallTest) ? (M + kRowsPerBlock - 1) / kRowsPerBlock : 0);
+  if (a.tiles == 0) return hipSuccess;
   a.test_group = H / test_kv_heads;
   a.alpha = alpha;
   a.q8_train = q8_train; a.q8_test = q8_test; a.k8 = k8; a.v8t = v8t;

@@ -22,15 +22,18 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #endif
 constexpr int kBlockKv = TFM_FP8_BLOCK_KV;  // keys per block (running-max granularity) of the FP8 kernel
 constexpr float kLog2e = 1.4426950408889634f;
+// Which of the two ICL calls an attention launch runs (a mask).
+constexpr int kCallTrain = 1, kCallTest = 2;
 
-// Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).
+// Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).  Everything
+// before q8_test depends on the train rows only (the state a fit call leaves behind).
 struct Fp8Workspace {
   size_t amax;      // 4*B*H uint32: |x| maxima of Q_train, K, V, Q_test as float bits
   size_t scales;    // 4*B*H float: s_q, s_k, s_v, s_q_test
   size_t q8_train;  // (B,H,N,D) codes
-  size_t q8_test;   // (B,H,M,D) codes
   size_t k8;        // (B,H,N,D) codes
   size_t v8t;       // (B,H,ceil(N/64),D,64) codes, tile-transposed (see attn_fp8.hip)
+  size_t q8_test;   // (B,H,M,D) codes
   size_t total;
 };
 Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M);
@@ -39,11 +42,11 @@ size_t v8t_bytes(int B, int H, int D, int N);
 // ---- launchers (return hipError_t of the launches) ----
 // Zero `n` uint32 words.
 hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s);
-// Per-(b,h) absmax of Q_train, K, V (and of Q_test when q_test is non-NULL and
-// M > 0) into amax[4][B][H] (must be zeroed first).
-hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, int M, const void* q_train,
-                       const void* k, const void* v, const void* q_test, uint32_t* amax,
-                       hipStream_t s);
+// Per-(b,h) absmax of tensors first..last of (Q_train, K, V, Q_test) into
+// amax[4][B][H] (those slots must be zeroed first); Q_test has M rows, the others N.
+hipError_t launch_amax(int in_bf16, int first, int last, int B, int H, int D, int N, int M,
+                       const void* q_train, const void* k, const void* v, const void* q_test,
+                       uint32_t* amax, hipStream_t s);
 // Scales from amax for a query-scale mode: s = fl32(amax/448), 1 where that is
 // 0; writes scales[4][B][H] (s_q, s_k, s_v, s_q_test) and, when the pointers are
 // non-NULL, copies them out.
@@ -58,8 +61,9 @@ hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, cons
 // Re-lay (B,H,N,D) V codes into the tile-transposed layout.
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8,
                                    uint8_t* v8t, hipStream_t s);
-// Fused FP8 attention over the N train and M test query rows of every (b,h).
-hipError_t launch_attn_fp8(int out_bf16, int B, int H, int D, int N, int M, int test_kv_heads,
+// Fused FP8 attention over the N train (calls & kCallTrain) and M test (calls & kCallTest)
+// query rows of every (b,h), all against the N train keys.
+hipError_t launch_attn_fp8(int out_bf16, int calls, int B, int H, int D, int N, int M, int test_kv_heads,
                            float alpha, const uint8_t* q8_train, const uint8_t* q8_test,
                            const uint8_t* k8, const uint8_t* v8t, const float* s_q,
                            const float* s_k, const float* s_v, const float* s_q_test,

@@ -78,13 +78,14 @@ struct RowMap {
 };
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void amax_kernel(int B, int H, int D, int N, int M, int rows_per_chunk,
+__global__ __launch_bounds__(kThreads) void amax_kernel(int first_tensor, int B, int H, int D, int N, int M,
+                                                        int rows_per_chunk,
                                                         const T* __restrict__ q, const T* __restrict__ k,
                                                         const T* __restrict__ v, const T* __restrict__ qt,
                                                         uint32_t* __restrict__ amax) {
   extern __shared__ uint32_t smax[];  // H entries
   constexpr int VEC = Vec<T>::n;
-  const int tensor = blockIdx.y, b = blockIdx.z;
+  const int tensor = first_tensor + blockIdx.y, b = blockIdx.z;
   const T* x = tensor == 0 ? q : (tensor == 1 ? k : (tensor == 2 ? v : qt));
   if (tensor == 3) N = M;   // the test queries have M rows
   if ((int)blockIdx.x * rows_per_chunk >= N) return;
@@ -285,21 +286,22 @@ hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_amax(int in_bf16, int B, int H, int D, int N, int M, const void* q_train, const void* k,
-                       const void* v, const void* q_test, uint32_t* amax, hipStream_t s) {
+hipError_t launch_amax(int in_bf16, int first, int last, int B, int H, int D, int N, int M, const void* q_train,
+                       const void* k, const void* v, const void* q_test, uint32_t* amax, hipStream_t s) {
+  if (last == 3 && M == 0) last = 2;   // no test rows to scan
+  if (last < first) return hipSuccess;
   const int esize = in_bf16 ? 2 : 4;
-  const int rows = M > N ? M : N;
-  const int rpc = chunk_rows(N, H, D, esize);
-  // tensors 0..2 (Q_train, K, V) always; tensor 3 (Q_test) only when its max is needed
-  dim3 grid((rows + rpc - 1) / rpc, (q_test && M > 0) ? 4 : 3, B);
+  const int rows = first == 3 ? M : ((last == 3 && M > N) ? M : N);   // the most rows of any launched tensor
+  const int rpc = chunk_rows(first == 3 ? M : N, H, D, esize);
+  dim3 grid((rows + rpc - 1) / rpc, last - first + 1, B);
   size_t lds = (size_t)H * sizeof(uint32_t);
   if (in_bf16)
-    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, B, H, D, N, M, rpc,
+    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, first, B, H, D, N, M, rpc,
                        (const uint16_t*)q_train, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)q_test,
                        amax);
   else
-    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, B, H, D, N, M, rpc, (const float*)q_train,
-                       (const float*)k, (const float*)v, (const float*)q_test, amax);
+    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, first, B, H, D, N, M, rpc,
+                       (const float*)q_train, (const float*)k, (const float*)v, (const float*)q_test, amax);
   return hipGetLastError();
 }
 

@@ -54,6 +54,10 @@ SIGNATURES = {
     "tfm_icl_attention_workspace_bytes": (_c_size, [_c_int] * 6),
     "tfm_icl_attention": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6
                           + [_c_int, ctypes.POINTER(_c_int), _p, _c_size, _p]),
+    "tfm_icl_attention_fp8_fit": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 4 + [_c_float] + [_p] * 5
+                                  + [_c_size, _p]),
+    "tfm_icl_attention_fp8_predict": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 3
+                                      + [_c_size, _p]),
     "tfm_noise_per_head_workspace_bytes": (_c_size, [_c_int] * 4),
     "tfm_noise_per_head": (_c_int, [_c_int] * 6 + [_p, _p, _c_float, _p, _p, _p, _c_size, _p]),
 }
@@ -282,6 +286,44 @@ def tfm_icl_attention_bf16(q_train, k, v, q_test=None, alpha=None, out_dtype=tor
           B, H, D, N, M, _alpha(alpha, D),
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
     return o_tr, o_te
+
+
+def tfm_icl_attention_fp8_fit(q_train, k, v, alpha=None, out_dtype=torch.float32, m_max=0, out=None,
+                              workspace=None, q_scale_mode="shared"):
+    """Quantize the train rows and run the train-train call; returns (o_train, workspace).
+
+    The workspace holds the fit state for tfm_icl_attention_fp8_predict, sized for test batches of up
+    to m_max rows (or pass a larger workspace)."""
+    B, N, H, D = _shape_bnhd(q_train, "q_train")
+    if tuple(k.shape) != (B, N, H, D) or tuple(v.shape) != (B, N, H, D):
+        raise ValueError("k and v must have the shape of q_train")
+    if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v}, q_train.dtype)
+    o_tr = out if out is not None else torch.empty((B, N, H, D), dtype=out_dtype, device=dev)
+    if tuple(o_tr.shape) != (B, N, H, D) or o_tr.dtype != out_dtype or not o_tr.is_contiguous():
+        raise ValueError("out must be a contiguous (B, N, H, D) tensor of the output dtype")
+    nws = tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, int(m_max))
+    ws = workspace if workspace is not None else torch.empty(nws, dtype=torch.uint8, device=dev)
+    _call("tfm_icl_attention_fp8_fit", _DTYPES[q_train.dtype], _DTYPES[out_dtype], _opts(q_scale_mode), B, H, D, N,
+          _alpha(alpha, D), _ptr(q_train), _ptr(k), _ptr(v), _ptr(o_tr), _ptr(ws), ws.numel(), _stream())
+    return o_tr, ws
+
+
+def tfm_icl_attention_fp8_predict(workspace, q_test, N, alpha=None, out_dtype=torch.float32, out=None,
+                                  q_scale_mode="shared", test_kv_heads=0):
+    """The test-train call for q_test (B, M, H, D) against the fit state in workspace (N train rows)."""
+    B, M, H, D = _shape_bnhd(q_test, "q_test")
+    if q_test.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_test": q_test if M else None, "workspace": workspace})
+    o_te = out if out is not None else torch.empty((B, M, H, D), dtype=out_dtype, device=dev)
+    if tuple(o_te.shape) != (B, M, H, D) or o_te.dtype != out_dtype or not o_te.is_contiguous():
+        raise ValueError("out must be a contiguous (B, M, H, D) tensor of the output dtype")
+    _call("tfm_icl_attention_fp8_predict", _DTYPES[q_test.dtype], _DTYPES[out_dtype],
+          _opts(q_scale_mode, test_kv_heads), B, H, D, int(N), M, _alpha(alpha, D), _ptr(q_test if M else None),
+          _ptr(o_te if M else None), _ptr(workspace), workspace.numel(), _stream())
+    return o_te
 
 
 FP8_MIN_TRAIN_ROWS_DEFAULT = 8192

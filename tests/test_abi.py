@@ -20,7 +20,7 @@ def header_functions():
 def test_library_exports_every_declared_function():
     L = tfm.lib()
     names = header_functions()
-    assert len(names) == 16
+    assert len(names) == 18
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(tfm.SIGNATURES)
@@ -156,3 +156,24 @@ def test_noise_validation_and_workspace():
     # fixed-order partial sums: one double per (row chunk, b, h), chunks of ceil(32768 / (H D)) rows, then rho
     assert ws(2, 6, 65536, 64) == ((65536 + 85) // 86 * 12 * 8 + 255) // 256 * 256 + 256
     assert ws(1, 1, 1, 8) == 512 and ws(1, 1, 0, 8) == 256 and ws(1, 1, 5, 12) == 0
+
+
+def test_fit_and_predict_validation():
+    L = tfm.lib()
+    f = lambda **kw: L.tfm_icl_attention_fp8_fit(1, 0, kw.get("o"), 1, 2, 64, kw.get("N", 300), kw.get("alpha", 0.1),
+                                                 FAKE, FAKE, kw.get("v", FAKE), kw.get("ot", FAKE), kw.get("ws", FAKE),
+                                                 kw.get("nws", 100), None)
+    # every call fails validation: the workspace of 100 bytes is always too small
+    assert f() == 6 and f(N=0) == 2 and f(alpha=0.0) == 8 and f(o=opts(mode=2)) == 8 and f(o=opts(g=3)) == 8
+    assert f(v=None) == 1 and f(ot=None) == 1 and f(ws=None) == 1 and f(v=MIS) == 5
+    need = tfm.tfm_icl_attention_fp8_workspace_bytes(1, 2, 64, 300, 0)
+    assert f(nws=need - 1) == 6
+    p = lambda **kw: L.tfm_icl_attention_fp8_predict(1, 0, kw.get("o"), 1, 2, 64, 300, kw.get("M", 50), 0.1,
+                                                     kw.get("qt", FAKE), kw.get("ot", FAKE), kw.get("ws", FAKE),
+                                                     kw.get("nws", 100), None)
+    assert p() == 6 and p(M=-1) == 2 and p(o=opts(mode=2)) == 8 and p(qt=None) == 1 and p(ot=MIS) == 5
+    assert p(M=0, qt=None, ot=None) == 6 and p(ws=None) == 1
+    # one byte short of what M = 50 needs still fails (never a valid call: the pointers are fake)
+    need_m = tfm.tfm_icl_attention_fp8_workspace_bytes(1, 2, 64, 300, 50)
+    assert need_m > tfm.tfm_icl_attention_fp8_workspace_bytes(1, 2, 64, 300, 0)
+    assert p(nws=need_m - 1) == 6
