@@ -69,6 +69,16 @@ def metrics(got, ref):
     return {"relF": float(np.linalg.norm(d) / np.linalg.norm(ref)), "max_abs_over_rms": float(d.max() / rms)}
 
 
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(x, w, rows, block_kv):
     """The oracle, single-threaded, on a bounded sample of the same workload; also returns
     its quantized codes and its O_qp rows (table 0, head 0) for the accuracy report."""
@@ -90,24 +100,28 @@ def cpu_baseline(x, w, rows, block_kv):
             "sample": "one-pass FP8 kernel model (fp64 numpy) for %d train query rows of table 0, head 0, "
                       "against all %d keys; quantization of that head (N+M rows) took %.2f s more" %
                       (rows, w.N, t_quant),
-            "seconds": round(t_attn, 2)}, o_qp[0, :, 0]
+            "seconds": round(t_attn, 2), "cpu_model": cpu_model()}, o_qp[0, :, 0], qz
 
 
-def accuracy(x, w, o_qp, gpu_fp8, gpu_bf16, rows):
+def accuracy(x, w, o_qp, qz, gpu_fp8, gpu_bf16, rows):
     """Errors on train rows [0, rows) of table 0, head 0: the FP8 kernel against the oracle's
-    kernel model (O_qp) and against unquantized fp64 attention (O_exact), the method's own
-    quantization error (O_qp against O_exact) and the bf16 kernel against O_exact."""
+    kernel model (O_qp), against Eq. (1) on the dequantized inputs (O_q) and against
+    unquantized fp64 attention (O_exact); the method's own error (O_qp and O_q against
+    O_exact); and the bf16 kernel against O_exact."""
     import numpy as np
     from oracle import attention as OA
 
     q = x["q_train"][0, :rows, 0].astype(np.float64)
     exact = OA.softmax_attention(q, x["k"][0, :, 0].astype(np.float64), x["v"][0, :, 0].astype(np.float64),
                                  float(w.alpha))
+    o_q = OA.icl_attention_dequantized(qz, w.alpha, np.arange(rows), [])[0][0, :, 0]
     qp = o_qp[:rows]
     out = {"rows": "train rows 0..%d of table 0, head 0 (fp32 outputs)" % (rows - 1),
            "fp8_kernel_vs_kernel_model": metrics(gpu_fp8, qp),
+           "fp8_kernel_vs_dequantized_fp64": metrics(gpu_fp8, o_q),
            "fp8_kernel_vs_fp64_exact": metrics(gpu_fp8, exact),
-           "kernel_model_vs_fp64_exact": metrics(qp, exact)}
+           "kernel_model_vs_fp64_exact": metrics(qp, exact),
+           "dequantized_vs_fp64_exact": metrics(o_q, exact)}
     if gpu_bf16 is not None:
         out["bf16_kernel_vs_fp64_exact"] = metrics(gpu_bf16, exact)
     return out
@@ -374,7 +388,7 @@ def main():
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) on %d rows" % args.cpu_rows)
         bkv = tfm.tfm_icl_attention_fp8_block_kv(w.D)
-        result["cpu_baseline"], o_qp = cpu_baseline(x, w, args.cpu_rows, bkv)
+        result["cpu_baseline"], o_qp, qz = cpu_baseline(x, w, args.cpu_rows, bkv)
         # one more FP8 call (and bf16 call) with fp32 outputs, outside the timed region
         f_tr, f_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha,
                                                workspace=ws)
@@ -386,7 +400,7 @@ def main():
                                                   alpha=w.alpha)[0][0, :r, 0].cpu().numpy()
         del f_tr, f_te
         log("accuracy on %d rows" % r)
-        result["accuracy"] = accuracy(x, w, o_qp, gpu_fp8, gpu_bf16, r)
+        result["accuracy"] = accuracy(x, w, o_qp, qz, gpu_fp8, gpu_bf16, r)
     print(json.dumps(result), flush=True)
 
 
