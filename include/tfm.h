@@ -10,7 +10,8 @@
  *     same N train keys and values);
  *   - Eq. (2): every tensor is quantized per head to OCP e4m3fn with a
  *     dynamic absmax scale s = max|X| / 448 and X_8 = rn(clamp(X/s, +-448));
- *     test queries reuse the scale of the train queries (batch invariance);
+ *     by default test queries reuse the scale of the train queries, which
+ *     makes each test row's output independent of its batch;
  *   - inside the fused kernel (Fig. 2): the Q and K scales are applied
  *     together with the softmax scale, P is lifted so that its row maximum is
  *     2^8 and rounded to e4m3, and the V scale is applied in the epilogue.
@@ -25,7 +26,8 @@
  *    for the call; they must be 16-byte aligned and must not alias each
  *    other.  A pointer whose element count is 0 (q_test / o_test / q8_test
  *    when M == 0) may be NULL.  The library never allocates device memory
- *    and keeps no state between calls, so calls are thread-safe.
+ *    and keeps no state between calls (a fit leaves its train state in the
+ *    caller's workspace), so calls are thread-safe.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream); no entry point synchronizes.
  *  - Every argument is validated before anything is enqueued; on error
@@ -124,7 +126,8 @@ int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, 
 
 /*
  * tfm_icl_attention_fp8 -- the full hot path: Eq. (2) quantization of
- * Q_train, K, V and Q_test (test queries on the train-query scale), then
+ * Q_train, K, V and Q_test (test queries on the train-query scale unless
+ * opts->q_scale_mode says otherwise), then
  * both ICL attention calls of Sec. 3 in one fused FP8 launch over the N + M
  * query rows, against the same quantized keys and values.
  *
@@ -162,12 +165,13 @@ int tfm_icl_attention_fp8(int in_dtype, int out_dtype, const tfm_icl_options* op
  * again on codes that are already in the workspace.
  *
  * tfm_icl_attention_fp8_quantize -- Eq. (2) for Q_train, K, V and Q_test
- *   (on the train-query scale) into `workspace`, in the private layout the
- *   attention stage reads (arguments as for tfm_icl_attention_fp8).
+ *   (Q_test on the scale opts->q_scale_mode selects) into `workspace`, in
+ *   the private layout the attention stage reads (arguments as for
+ *   tfm_icl_attention_fp8; only q_scale_mode of opts is used).
  * tfm_icl_attention_fp8_attend -- both ICL calls from a workspace filled by
- *   tfm_icl_attention_fp8_quantize with the same B, H, D, N, M and query-
- *   scale mode; the workspace is only read.  Outputs as for
- *   tfm_icl_attention_fp8.
+ *   tfm_icl_attention_fp8_quantize with the same B, H, D, N, M; the scales
+ *   it uses are the ones stored there, so only test_kv_heads of opts is
+ *   used; the workspace is only read.  Outputs as for tfm_icl_attention_fp8.
  */
 int tfm_icl_attention_fp8_quantize(int in_dtype, const tfm_icl_options* opts, int B, int H, int D,
                                    int N, int M,

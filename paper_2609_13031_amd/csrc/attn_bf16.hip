@@ -5,6 +5,7 @@
 // with the same structure, without quantization:
 //  * a workgroup of 4 wave64s owns 128 train rows or 128 test rows of one
 //    (b, h); 32 per wave; test rows may attend to a shared K/V head;
+//  * fp32 inputs are rounded to bf16 (nearest even) as they are loaded;
 //  * key blocks of kBlockKvBf16 keys; K and V are staged through LDS in their
 //    row-major bf16 layout (double-buffered, one barrier per block);
 //  * S^T = K Q^T with v_mfma_f32_32x32x16_bf16, so each lane holds the scores

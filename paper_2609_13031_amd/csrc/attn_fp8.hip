@@ -3,15 +3,24 @@
 // The kernel of Sec. 3 / Fig. 2 of the paper, laid out for CDNA4:
 //  * a workgroup of 4 wave64s owns 128 consecutive train rows or 128
 //    consecutive test rows of one (b, h) (both ICL calls share K_8 and V_8,
-//    so they are one launch); each wave owns 32 rows; test rows may attend to
-//    a shared K/V head (grouped-query test-train call);
-//  * key tiles of 64 are staged through LDS; per tile each wave computes
-//    S^T = K_8 Q_8^T with two v_mfma_f32_32x32x64_f8f6f4 per 64 of head_dim
-//    (fp32 accumulation), so every lane holds 32 scores of one query row;
-//  * online softmax in the exp2 domain: running max m, P~ = 2^(c S + 8 - c m)
-//    with c = alpha * s_q * s_k * log2(e) (the Q and K scales applied with the
-//    softmax scale), so the running row maximum maps to 2^8; P~ is rounded
-//    to e4m3 by v_cvt_pk_fp8_f32 (round to nearest even);
+//    so they are one launch; the grid lists the train tiles of each (b, h),
+//    then its test tiles, and a launch may run only one of the two calls);
+//    each wave owns 32 rows; test rows may attend to a shared K/V head
+//    (grouped-query test-train call);
+//  * keys are processed in blocks of kBlockKv (128), staged through LDS with
+//    double buffering: the global loads of block k+1 are issued before the
+//    math of block k and written to the other buffer after it, one barrier
+//    per block;
+//  * per 32-key tile each wave computes S^T = K_8 Q_8^T with
+//    v_mfma_f32_32x32x64_f8f6f4 (fp32 accumulation; two per 64 of head_dim),
+//    so every lane holds 32 scores of one query row, and the two lanes of a
+//    row exchange their maxima with v_permlane32_swap;
+//  * online softmax in the exp2 domain with one running max per block: P~ =
+//    2^(c S + 8 - c m) with c = alpha * s_q * s_k * log2(e) (the Q and K
+//    scales applied with the softmax scale), so the running row maximum maps
+//    to 2^8; P~ is rounded to e4m3 by v_cvt_pk_fp8_f32 (round to nearest
+//    even); the state is rescaled only in blocks where some row's max grew,
+//    and a block whose lifted weights all round to zero is skipped exactly;
 //  * the e4m3 P tile of the QK^T accumulator is directly the B operand of
 //    O^T += V_8^T P_8^T (v_mfma_f32_32x32x64_f8f6f4): V is stored
 //    tile-transposed with its keys in the accumulator's row order, so no
@@ -19,6 +28,8 @@
 //  * the row sum l = sum P_8 comes from one v_mfma_f32_16x16x128_f8f6f4 of a
 //    constant 0/1 operand against the same P_8 operand;
 //  * epilogue: O * s_v / l (the V scale applied last), fp32 or bf16 out.
+// The VALU work per score (fma, exp, convert, max) bounds the kernel at head
+// dimension 64; the MFMAs run beside it.
 #include "common.h"
 
 namespace tfm {
