@@ -40,8 +40,13 @@ def log(*a):
 
 
 def source_digest(name):
-    with open(os.path.join(CSRC, name), "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    """Hash of a kernel source's code: comments and blank lines do not count."""
+    import re
+    with open(os.path.join(CSRC, name)) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    lines = [re.sub(r"//.*", "", line).strip() for line in text.splitlines()]
+    return hashlib.sha256("\n".join(x for x in lines if x).encode()).hexdigest()[:16]
 
 
 def counter_value(key, source):

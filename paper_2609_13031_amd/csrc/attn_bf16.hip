@@ -201,6 +201,8 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
           if (kb * BKV + 32 * t + (r / 4) * 8 + half * 4 + (r % 4) >= N) st[t][r] = -__builtin_inff();
     }
 
+    // softmax part at raised wave priority, as in the FP8 kernel
+    __builtin_amdgcn_s_setprio(1);
     float mx = st[0][0];
 #pragma unroll
     for (int t = 0; t < NS; ++t)
@@ -242,6 +244,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
       }
     }
 
+    __builtin_amdgcn_s_setprio(0);
     if (more) {
       uint8_t* nk = lds + ((kb + 1) & 1) * 2 * TBYTES;
       stage_store<D, BKV>(nk, nk + TBYTES, kr, vr);

@@ -200,6 +200,9 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
     }
 
     // ---- running max over the block; rescale the state by 2^(c (m_old - m_new)) ----
+    // The softmax part runs at raised wave priority: where waves of a SIMD compete for
+    // issue, the one with VALU work goes first while the others' MFMAs proceed.
+    __builtin_amdgcn_s_setprio(1);
     float mx = st[0][0];
 #pragma unroll
     for (int t = 0; t < NS; ++t)
@@ -252,6 +255,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
       }
     }  // not skipped
 
+    __builtin_amdgcn_s_setprio(0);
     if (more) {
       uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
       stage_store<D, BKV>(nk, nk + KBYTES, kr, vr);

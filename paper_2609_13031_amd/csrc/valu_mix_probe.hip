@@ -36,7 +36,8 @@ typedef float v16f __attribute__((ext_vector_type(16)));
 #define MAX3(i) asm volatile("v_max3_f32 %0, %0, %1, %1" : "+v"(a[i]) : "v"(a[(i + 1) & 15]));
 
 // MODE 0..3: one instruction x16 per step; 4: four 32x32x64 FP8 MFMAs per step;
-// 5: the per-score mix for 16 scores per lane; 6: the mix plus its 2 MFMAs.
+// 5: the per-score mix for 16 scores per lane; 6: the mix plus its 2 MFMAs at
+// head_dim 64; 7: the mix plus its 4 MFMAs at head_dim 128.
 template <int MODE>
 __global__ __launch_bounds__(256) void probe(float* out, int iters, float seed) {
   float a[16];
@@ -60,11 +61,15 @@ __global__ __launch_bounds__(256) void probe(float* out, int iters, float seed) 
       acc0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opa, opb, acc0, 0, 0, 0, 0, 0, 0);
       acc1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opb, opa, acc1, 0, 0, 0, 0, 0, 0);
     }
-    if (MODE == 5 || MODE == 6) {
+    if (MODE == 5 || MODE == 6 || MODE == 7) {
       R16(MAX3) R16(FMA) R16(EXP)
       CVTH(0) CVTH(1) CVTH(2) CVTH(3) CVTH(4) CVTH(5) CVTH(6) CVTH(7)
     }
-    if (MODE == 6) {
+    if (MODE == 6 || MODE == 7) {
+      acc0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opa, opb, acc0, 0, 0, 0, 0, 0, 0);
+      acc1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opb, opa, acc1, 0, 0, 0, 0, 0, 0);
+    }
+    if (MODE == 7) {
       acc0 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opa, opb, acc0, 0, 0, 0, 0, 0, 0);
       acc1 = __builtin_amdgcn_mfma_scale_f32_32x32x64_f8f6f4(opb, opa, acc1, 0, 0, 0, 0, 0, 0);
     }
@@ -98,19 +103,22 @@ int main() {
   float* d;
   CK(hipMalloc(&d, (size_t)blocks * 256 * sizeof(float)));
   const char* names[] = {"v_fma_f32", "v_exp_f32", "v_cvt_pk_fp8_f32", "v_max3_f32", "v_mfma_f32_32x32x64_f8f6f4",
-                         "mix: 16 fma + 16 exp + 8 cvt + 16 max3", "mix + 2 MFMA 32x32x64 f8"};
-  float ms[7] = {run<0>(d, blocks, iters), run<1>(d, blocks, iters), run<2>(d, blocks, iters),
+                         "mix: 16 fma + 16 exp + 8 cvt + 16 max3", "mix + 2 MFMA 32x32x64 f8 (D = 64)",
+                         "mix + 4 MFMA 32x32x64 f8 (D = 128)"};
+  float ms[8] = {run<0>(d, blocks, iters), run<1>(d, blocks, iters), run<2>(d, blocks, iters),
                  run<3>(d, blocks, iters), run<4>(d, blocks, iters), run<5>(d, blocks, iters),
-                 run<6>(d, blocks, iters)};
+                 run<6>(d, blocks, iters), run<7>(d, blocks, iters)};
   const double scores = (double)blocks * 256 * iters * 16;  // scores per mix run (16 per lane per step)
-  for (int m = 0; m < 7; ++m) {
+  for (int m = 0; m < 8; ++m) {
     const double cyc_step = ms[m] * 2.4e6 / iters;          // per SIMD, 2.4 GHz cycles
     const double per_instr = cyc_step / (4.0 * (m == 4 ? 4.0 : 16.0));
     printf("%-42s %8.3f ms", names[m], ms[m]);
     if (m < 5) printf("  %6.2f cycles per wave64 instruction", per_instr);
-    if (m >= 5)
-      printf("  -> %.4g scores/s = %.0f TFLOP/s at head_dim 64 (256 flop per score)", scores / (ms[m] * 1e-3),
-             scores / (ms[m] * 1e-3) * 256 / 1e12);
+    if (m >= 5) {
+      const int d = m == 7 ? 128 : 64;
+      printf("  -> %.4g scores/s = %.0f TFLOP/s at head_dim %d (%d flop per score)", scores / (ms[m] * 1e-3),
+             scores / (ms[m] * 1e-3) * 4 * d / 1e12, d, 4 * d);
+    }
     printf("\n");
   }
   CK(hipFree(d));
