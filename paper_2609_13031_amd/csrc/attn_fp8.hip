@@ -38,7 +38,9 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
 constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
-constexpr int kPad = 16;  // LDS row padding (bytes): conflict-free 16-byte lane reads
+constexpr int kPad = 16;  // padded-layout LDS row padding (bytes): conflict-free 16-byte lane reads
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(1))) void global_void;
 
 struct Fp8Args {
   int B, H, N, M;
@@ -83,6 +85,57 @@ __device__ inline int pack4_e4m3(float p0, float p1, float p2, float p3) {
   return __builtin_amdgcn_cvt_pk_fp8_f32(p2, p3, lo, true);
 }
 
+// LDS rows of RB bytes hold 16-byte chunks XOR-swizzled instead of padded
+// (the DMA below writes 1024 contiguous bytes per wave instruction): chunk c
+// of row r sits at chunk position c ^ swz(r), which keeps the 16-byte MFMA
+// operand reads free of bank conflicts (measured for both row sizes).
+template <int RB>
+__device__ inline int swz(int r) {
+  static_assert(RB == 64 || RB == 128, "rows of 64 or 128 bytes");
+  return RB == 64 ? (r >> 2) & 3 : (r >> 1) & 7;
+}
+template <int RB>
+__device__ inline int lds_off(int r, int c) {
+  return r * RB + ((c ^ swz<RB>(r)) << 4);
+}
+// Copy key block kb straight from global memory into LDS (global_load_lds_dwordx4:
+// lane l of a wave instruction writes LDS bytes [base + 16 l, +16)): K as BKV rows
+// of D bytes, V^T as BKV/64 stacked tiles of D rows of 64 bytes.  The 1024-byte
+// pieces are shared out over the 4 waves.  Keys >= N read row N-1 and 64-key tiles
+// past the end read the last tile: their scores are masked to -inf, so their
+// weights are exactly 0.
+template <int D, int BKV>
+__device__ inline void stage_dma(const uint8_t* kbase, const uint8_t* vbase, int kb, int N, int ntiles64,
+                                 uint8_t* k_lds, uint8_t* v_lds, int wave, int lane) {
+  constexpr int NP = BKV / 64;
+  constexpr int KPIECES = BKV * D / 1024, VPIECES = NP * D * 64 / 1024;
+  static_assert(KPIECES % kWaves == 0 && VPIECES % kWaves == 0, "pieces split evenly over the waves");
+#pragma unroll
+  for (int i = 0; i < KPIECES / kWaves; ++i) {
+    const int j = wave + kWaves * i;
+    const int at = j * 1024 + lane * 16;
+    const int r = at / D, pos = (at % D) >> 4;
+    const int key = min(kb * BKV + r, N - 1);
+    const uint8_t* g = kbase + (size_t)key * D + ((pos ^ swz<D>(r)) << 4);
+    __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(k_lds + j * 1024), 16, 0, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < VPIECES / kWaves; ++i) {
+    const int j = wave + kWaves * i;
+    const int at = j * 1024 + lane * 16;
+    const int r = at / 64, pos = (at % 64) >> 4;           // r = p * D + d
+    const int t64 = min(kb * NP + r / D, ntiles64 - 1);
+    const uint8_t* g = vbase + (size_t)t64 * D * 64 + (r % D) * 64 + ((pos ^ swz<64>(r)) << 4);
+    __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(v_lds + j * 1024), 16, 0, 0);
+  }
+}
+
+// Wait for this wave's outstanding DMA into LDS (vmcnt(0)), before the barrier
+// after which other waves read it.
+__device__ inline void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// The other staging scheme (used at D = 64, where it measured faster): registers,
+// then padded LDS rows (row stride RB + kPad).
 // Stage one key block (BKV keys) of K (row-major, rows >= N read as zero) and
 // V^T (BKV/64 tiles of D x 64 bytes, tiles past the end read as zero) into
 // registers, 16 bytes per thread per piece.
@@ -115,14 +168,29 @@ __device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* 
   }
 }
 
+// Offset of 16-byte chunk c of LDS row r, in the swizzled (SWZ) or the padded layout.
+template <int RB, bool SWZ>
+__device__ inline int row_chunk(int r, int c) {
+  if constexpr (SWZ) return lds_off<RB>(r, c);
+  else return r * (RB + kPad) + (c << 4);
+}
+// 32 bytes of LDS row r starting at (even) chunk c0.
+template <int RB, bool SWZ>
+__device__ inline v8i load32_lds(const uint8_t* base, int r, int c0) {
+  const u32x4 x = *reinterpret_cast<const u32x4*>(base + row_chunk<RB, SWZ>(r, c0));
+  const u32x4 y = *reinterpret_cast<const u32x4*>(base + row_chunk<RB, SWZ>(r, c0 + 1));
+  return v8i{(int)x.x, (int)x.y, (int)x.z, (int)x.w, (int)y.x, (int)y.y, (int)y.z, (int)y.w};
+}
+
 template <int D, int BKV, bool OUT_BF16>
 __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   constexpr int KD = D / 64;            // 64-wide head_dim chunks (k of one MFMA)
   constexpr int NS = BKV / 32;          // 32-key score tiles per key block
   constexpr int NP = BKV / 64;          // 64-key PV chunks per key block
-  constexpr int KS = D + kPad;          // K row stride in LDS
-  constexpr int VS = 64 + kPad;         // V^T row stride in LDS
-  constexpr int KBYTES = BKV * KS, VBYTES = NP * D * VS;
+  // D = 128: K/V copied into LDS by DMA, swizzled rows; D = 64: staged through
+  // registers into padded rows (each measured the faster at its head dimension)
+  constexpr bool kDma = D == 128;
+  constexpr int KBYTES = BKV * (kDma ? D : D + kPad), VBYTES = NP * D * (kDma ? 64 : 64 + kPad);
   constexpr int PIECES = BKV * D / 16 / 256;
   // two K/V stages: the next key block is written while the current one is read
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * (KBYTES + VBYTES)];
@@ -171,16 +239,28 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   const uint8_t* kbase = a.k8 + (size_t)bhkv * N * D;
   const uint8_t* vbase = a.v8t + (size_t)bhkv * ntiles64 * D * 64;
 
-  u32x4 kr[PIECES], vr[PIECES];
-  stage_load<D, BKV>(kbase, vbase, 0, N, ntiles64, kr, vr);
-  stage_store<D, BKV>(lds, lds + KBYTES, kr, vr);
+  u32x4 kr[kDma ? 1 : PIECES], vr[kDma ? 1 : PIECES];
+  if constexpr (kDma) {
+    stage_dma<D, BKV>(kbase, vbase, 0, N, ntiles64, lds, lds + KBYTES, wave, lane);
+    wait_dma();
+  } else {
+    stage_load<D, BKV>(kbase, vbase, 0, N, ntiles64, kr, vr);
+    stage_store<D, BKV>(lds, lds + KBYTES, kr, vr);
+  }
   __syncthreads();
 
   for (int kb = 0; kb < nblocks; ++kb) {
     uint8_t* k_lds = lds + (kb & 1) * (KBYTES + VBYTES);
     uint8_t* v_lds = k_lds + KBYTES;
     const bool more = kb + 1 < nblocks;
-    if (more) stage_load<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
+    if (more) {
+      if constexpr (kDma) {
+        uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
+        stage_dma<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
+      } else {
+        stage_load<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
+      }
+    }
 
     // ---- S^T = K_8 Q_8^T, 32 keys per accumulator tile ----
     v16f st[NS];
@@ -188,7 +268,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
     for (int t = 0; t < NS; ++t) {
       st[t] = v16f{};
 #pragma unroll
-      for (int s = 0; s < KD; ++s) st[t] = mfma_f8_32x32x64(load32(k_lds + (32 * t + ql) * KS + 64 * s + 32 * half), qf[s], st[t]);
+      for (int s = 0; s < KD; ++s) st[t] = mfma_f8_32x32x64(load32_lds<D, kDma>(k_lds, 32 * t + ql, 4 * s + 2 * half), qf[s], st[t]);
     }
     // keys beyond N (last block only) take no part
     if (kb * BKV + BKV > N) {
@@ -251,12 +331,14 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
         lacc = mfma_f8_16x16x128(ones, pf[p], lacc);
 #pragma unroll
         for (int i = 0; i < D / 32; ++i)
-          acc_o[i] = mfma_f8_32x32x64(load32(v_lds + (p * D + 32 * i + ql) * VS + 32 * half), pf[p], acc_o[i]);
+          acc_o[i] = mfma_f8_32x32x64(load32_lds<64, kDma>(v_lds, p * D + 32 * i + ql, 2 * half), pf[p], acc_o[i]);
       }
     }  // not skipped
 
     __builtin_amdgcn_s_setprio(0);
-    if (more) {
+    if constexpr (kDma) {
+      wait_dma();
+    } else if (more) {
       uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
       stage_store<D, BKV>(nk, nk + KBYTES, kr, vr);
     }
