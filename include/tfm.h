@@ -30,10 +30,11 @@
  *    caller's workspace), so calls are thread-safe.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream); no entry point synchronizes.
- *  - Every argument is validated before anything is enqueued; on error
- *    nothing is enqueued and a tfm_status other than TFM_OK is returned.
- *    TFM_ERR_HIP means the HIP runtime refused a launch.  No C++ exception
- *    crosses this interface.
+ *  - Every argument is validated before anything is enqueued; on a
+ *    validation error nothing is enqueued and a tfm_status other than TFM_OK
+ *    is returned.  TFM_ERR_HIP means the HIP runtime refused a launch; the
+ *    launches of the same call before it may already be enqueued, so the
+ *    outputs are then unspecified.  No C++ exception crosses this interface.
  *  - Inputs must be finite; for non-finite inputs the results are
  *    unspecified.
  */

@@ -37,8 +37,9 @@ using namespace tfm;
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Shapes every entry point accepts.  Limits: B*H <= 65535 (a grid dimension),
-// N + M below INT_MAX - 256 (row indices are 32-bit), B*H*ceil((N+M)/128)
-// workgroups at most INT_MAX, and B*H*D*(N+M) elements at most 2^48.
+// N + M below INT_MAX - 256 (row indices are 32-bit), B*H*(ceil(N/128) +
+// ceil(M/128)) attention workgroups at most INT_MAX, and B*H*D*(N+M) elements
+// at most 2^48.
 int check_shape(int B, int H, int D, int N, int M) {
   if (B < 1 || H < 1 || N < 1 || M < 0) return TFM_ERR_BAD_SHAPE;
   if ((long long)B * H > 65535) return TFM_ERR_BAD_SHAPE;

@@ -121,6 +121,8 @@ def _check_inputs(tensors, dtype=None):
             dev = t.device
         elif t.device != dev:
             raise ValueError("all tensors must be on one device")
+    if dev is not None and dev.index is not None and dev.index != torch.cuda.current_device():
+        raise ValueError("tensors must be on the current device (the library enqueues on its current stream)")
     return dev
 
 
