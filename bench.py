@@ -29,10 +29,10 @@ COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
 CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
 HBM_PEAK_GBS = 8000.0
 # The FP8 kernel's VALU work per (query, key) score is one v_fma_f32, one v_exp_f32, half a
-# v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (3.29, 8.66, 8.84 and
-# 5.67 cycles per wave64 instruction) over 1024 SIMDs at 2.4 GHz give this many scores per
+# v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (3.29, 8.68, 8.82 and
+# 5.64 cycles per wave64 instruction) over 1024 SIMDs at 2.4 GHz give this many scores per
 # second at most, i.e. 4*D times it in FLOP/s.
-ALU_SCORES_PER_S = 1024 * 2.4e9 * 64 / (3.29 + 8.66 + 8.84 / 2 + 5.67 / 2)
+ALU_SCORES_PER_S = 1024 * 2.4e9 * 64 / (3.29 + 8.68 + 8.82 / 2 + 5.64 / 2)
 
 
 def log(*a):
