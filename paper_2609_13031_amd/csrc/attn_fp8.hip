@@ -138,8 +138,10 @@ __device__ inline void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // then padded LDS rows (row stride RB + kPad).
 // Stage one key block (BKV keys) of K (row-major, rows >= N read as zero) and
 // V^T (BKV/64 tiles of D x 64 bytes, tiles past the end read as zero) into
-// registers, 16 bytes per thread per piece.
-template <int D, int BKV>
+// registers, 16 bytes per thread per piece.  FULL: the caller knows the whole
+// block lies below N, so the loads go unpredicated (no per-block compares and
+// zero fills on all but the last block).
+template <int D, int BKV, bool FULL = false>
 __device__ inline void stage_load(const uint8_t* kbase, const uint8_t* vbase, int kb, int N, int ntiles64,
                                   u32x4* kr, u32x4* vr) {
   constexpr int PIECES = BKV * D / 16 / 256;
@@ -148,10 +150,12 @@ __device__ inline void stage_load(const uint8_t* kbase, const uint8_t* vbase, in
     const int i = threadIdx.x + 256 * j;
     const int r = i / (D / 16), cc = i % (D / 16);
     const int key = kb * BKV + r;
-    kr[j] = key < N ? *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16) : u32x4{0u, 0u, 0u, 0u};
+    kr[j] = (FULL || key < N) ? *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16)
+                              : u32x4{0u, 0u, 0u, 0u};
     const int t64 = kb * (BKV / 64) + i / (D * 4);          // 64-key tile of this piece
-    vr[j] = t64 < ntiles64 ? *reinterpret_cast<const u32x4*>(vbase + (size_t)t64 * D * 64 + (i % (D * 4)) * 16)
-                           : u32x4{0u, 0u, 0u, 0u};
+    vr[j] = (FULL || t64 < ntiles64)
+                ? *reinterpret_cast<const u32x4*>(vbase + (size_t)t64 * D * 64 + (i % (D * 4)) * 16)
+                : u32x4{0u, 0u, 0u, 0u};
   }
 }
 
@@ -257,6 +261,8 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
       if constexpr (kDma) {
         uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
         stage_dma<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
+      } else if ((kb + 2) * BKV <= N) {
+        stage_load<D, BKV, true>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
       } else {
         stage_load<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
       }
