@@ -385,7 +385,7 @@ def main():
                          "peak": round(ALU_SCORES_PER_S * 4 * w.D / 1e12, 1), "unit": "TFLOP/s",
                          "frac": round(achieved / (ALU_SCORES_PER_S * 4 * w.D / 1e12), 4),
                          "note": "VALU issue ceiling of the softmax work per score (exp, fma, e4m3 convert, max)"},
-        "quantize_hbm": {"stage": "amax + scales + codes of Q_train, K, V, Q_test (5 launches)",
+        "quantize_hbm": {"stage": "slice maxima, then scales and codes of Q_train, K, V, Q_test (2 launches)",
                          "ms": round(quant_ms, 4), "algorithmic_bytes": q_algo, "achieved": round(q_gbs, 1),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(q_gbs / HBM_PEAK_GBS, 4),
                          "traffic": counter_value("quantize_stage_hbm_bytes_per_step", "quantize.hip")},

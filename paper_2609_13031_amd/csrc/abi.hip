@@ -18,7 +18,7 @@ Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M) {
   Fp8Workspace w;
   const size_t bh = (size_t)B * H;
   size_t off = 0;
-  w.amax = off;      off += align256(4 * bh * sizeof(uint32_t));
+  w.amax = off;      off += align256(amax_partial_words(B, H) * sizeof(uint32_t));
   w.scales = off;    off += align256(4 * bh * sizeof(float));
   w.q8_train = off;  off += align256(bh * N * D);
   w.k8 = off;        off += align256(bh * N * D);
@@ -86,25 +86,18 @@ int hip_status(hipError_t e) { return e == hipSuccess ? TFM_OK : TFM_ERR_HIP; }
 #define TFM_TRY(expr) do { int st_ = (expr); if (st_ != TFM_OK) return st_; } while (0)
 #define TFM_HIP(expr) do { if ((expr) != hipSuccess) return TFM_ERR_HIP; } while (0)
 
-// amax + scales + the four code tensors.  v8 == nullptr writes V to v8t instead.
-// amax holds 4*B*H words and scales 4*B*H floats (s_q, s_k, s_v, s_q_test).
+// Slice maxima, then scales and the four code tensors in one launch.  v8 == nullptr
+// writes V to v8t instead.  partial holds amax_partial_words(B, H) words and scales
+// 4*B*H floats (s_q, s_k, s_v, s_q_test).
 int quantize_all(int in_dtype, int q_scale_mode, int B, int H, int D, int N, int M, const void* q_train,
                  const void* k, const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8, uint8_t* v8,
-                 uint8_t* v8t, uint8_t* q8_test, uint32_t* amax, float* scales, float* s_q, float* s_k, float* s_v,
-                 float* s_q_test, hipStream_t s) {
+                 uint8_t* v8t, uint8_t* q8_test, uint32_t* partial, float* scales, float* s_q, float* s_k,
+                 float* s_v, float* s_q_test, hipStream_t s) {
   const int bf = in_dtype == TFM_BF16;
-  const int BH = B * H;
   const bool test_amax = q_scale_mode != TFM_QSCALE_SHARED && M > 0;
-  TFM_HIP(launch_fill_zero_u32(amax, 4 * BH, s));
-  TFM_HIP(launch_amax(bf, 0, test_amax ? 3 : 2, B, H, D, N, M, q_train, k, v, q_test, amax, s));
-  TFM_HIP(launch_scales(BH, q_scale_mode, amax, scales, s_q, s_k, s_v, s_q_test, s));
-  // V, K, then the queries: the reverse of the order the amax pass read them in, so the
-  // second read of the most recently scanned tensors can still hit the memory-side cache
-  if (v8) TFM_HIP(launch_quantize_rows(bf, B, H, D, N, v, scales + 2 * BH, v8, s));
-  else TFM_HIP(launch_quantize_v_tiles(bf, B, H, D, N, v, scales + 2 * BH, v8t, s));
-  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, k, scales + BH, k8, s));
-  TFM_HIP(launch_quantize_rows(bf, B, H, D, N, q_train, scales, q8_train, s));
-  if (M > 0) TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, q8_test, s));
+  TFM_HIP(launch_amax(bf, 0, test_amax ? 3 : 2, B, H, D, N, M, q_train, k, v, q_test, partial, s));
+  TFM_HIP(launch_quantize(bf, q_scale_mode, B, H, D, N, M, q_train, k, v, M > 0 ? q_test : nullptr, q8_train, k8,
+                          v8, v8 ? nullptr : v8t, q8_test, partial, scales, s_q, s_k, s_v, s_q_test, s));
   return TFM_OK;
 }
 
@@ -133,8 +126,8 @@ const char* tfm_status_string(int status) {
 int tfm_version(void) { return 200; }
 
 size_t tfm_quantize_workspace_bytes(int B, int H) {
-  if (B < 1 || H < 1) return 0;
-  return align256(4 * (size_t)B * H * sizeof(uint32_t)) + align256(4 * (size_t)B * H * sizeof(float));
+  if (B < 1 || H < 1 || (long long)B * H > 65535) return 0;
+  return align256(amax_partial_words(B, H) * sizeof(uint32_t)) + align256(4 * (size_t)B * H * sizeof(float));
 }
 
 int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, int H, int D, int N, int M,
@@ -153,7 +146,7 @@ int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, 
   if (workspace_bytes < tfm_quantize_workspace_bytes(B, H)) return TFM_ERR_WORKSPACE_TOO_SMALL;
   uint8_t* ws = (uint8_t*)workspace;
   uint32_t* amax = (uint32_t*)ws;
-  float* scales = (float*)(ws + align256(4 * (size_t)B * H * sizeof(uint32_t)));
+  float* scales = (float*)(ws + align256(amax_partial_words(B, H) * sizeof(uint32_t)));
   return quantize_all(in_dtype, o.q_scale_mode, B, H, D, N, M, q_train, k, v, q_test, q8_train, k8, v8, nullptr,
                       q8_test, amax, scales, s_q, s_k, s_v, s_q_test, (hipStream_t)stream);
 }
@@ -270,13 +263,12 @@ int tfm_icl_attention_fp8_predict(int in_dtype, int out_dtype, const tfm_icl_opt
   float* scales = (float*)(ws + L.scales);
   const int bf = in_dtype == TFM_BF16;
   const int BH = B * H;
-  if (o.q_scale_mode == TFM_QSCALE_PER_CALL) {
-    TFM_HIP(launch_fill_zero_u32(amax + 3 * BH, BH, s));
+  if (o.q_scale_mode == TFM_QSCALE_PER_CALL)
     TFM_HIP(launch_amax(bf, 3, 3, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, amax, s));
-  }
-  // the train slots of amax are the fit's, so s_q, s_k and s_v come out as they did then
-  TFM_HIP(launch_scales(BH, o.q_scale_mode, amax, scales, nullptr, nullptr, nullptr, nullptr, s));
-  TFM_HIP(launch_quantize_rows(bf, B, H, D, M, q_test, scales + 3 * BH, ws + L.q8_test, s));
+  // Under the shared scale s_q_test comes from the fit's Q_train slice maxima, which the
+  // workspace still holds; s_q, s_k and s_v stay as the fit stored them.
+  TFM_HIP(launch_quantize(bf, o.q_scale_mode, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, nullptr, nullptr,
+                          nullptr, nullptr, ws + L.q8_test, amax, scales, nullptr, nullptr, nullptr, nullptr, s));
   return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTest, B, H, D, N, M, o.test_kv_heads, alpha,
                                     ws + L.q8_train, ws + L.q8_test, ws + L.k8, ws + L.v8t, scales, scales + BH,
                                     scales + 2 * BH, scales + 3 * BH, nullptr, o_test, s));

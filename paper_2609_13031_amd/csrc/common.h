@@ -25,10 +25,24 @@ constexpr float kLog2e = 1.4426950408889634f;
 // Which of the two ICL calls an attention launch runs (a mask).
 constexpr int kCallTrain = 1, kCallTest = 2;
 
+// The amax pass splits the rows of each (tensor, table) into at most kAmaxSlices
+// slices of at least kMinSliceRows rows and keeps one maximum per (slice, head).
+constexpr int kAmaxSlices = 128;
+constexpr int kMinSliceRows = 16;
+__host__ __device__ inline int amax_slice_rows(int rows) {
+  const int r = (rows + kAmaxSlices - 1) / kAmaxSlices;
+  return r < kMinSliceRows ? kMinSliceRows : r;
+}
+__host__ __device__ inline int amax_slices(int rows) {
+  return rows <= 0 ? 0 : (rows + amax_slice_rows(rows) - 1) / amax_slice_rows(rows);
+}
+// uint32 words of the slice maxima of the four tensors: [4][B][H][kAmaxSlices]
+inline size_t amax_partial_words(int B, int H) { return (size_t)4 * B * H * kAmaxSlices; }
+
 // Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).  Everything
 // before q8_test depends on the train rows only (the state a fit call leaves behind).
 struct Fp8Workspace {
-  size_t amax;      // 4*B*H uint32: |x| maxima of Q_train, K, V, Q_test as float bits
+  size_t amax;      // [4][B][H][kAmaxSlices] uint32: slice maxima of |x| (float bits) of Q_train, K, V, Q_test
   size_t scales;    // 4*B*H float: s_q, s_k, s_v, s_q_test
   size_t q8_train;  // (B,H,N,D) codes
   size_t k8;        // (B,H,N,D) codes
@@ -42,22 +56,22 @@ size_t v8t_bytes(int B, int H, int D, int N);
 // ---- launchers (return hipError_t of the launches) ----
 // Zero `n` uint32 words.
 hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s);
-// Per-(b,h) absmax of tensors first..last of (Q_train, K, V, Q_test) into
-// amax[4][B][H] (those slots must be zeroed first); Q_test has M rows, the others N.
+// Slice maxima of |x| per head of tensors first..last of (Q_train, K, V, Q_test) into
+// partial[4][B][H][kAmaxSlices]; Q_test has M rows, the others N.
 hipError_t launch_amax(int in_bf16, int first, int last, int B, int H, int D, int N, int M,
                        const void* q_train, const void* k, const void* v, const void* q_test,
-                       uint32_t* amax, hipStream_t s);
-// Scales from amax for a query-scale mode: s = fl32(amax/448), 1 where that is
-// 0; writes scales[4][B][H] (s_q, s_k, s_v, s_q_test) and, when the pointers are
-// non-NULL, copies them out.
-hipError_t launch_scales(int BH, int q_scale_mode, const uint32_t* amax, float* scales, float* s_q,
-                         float* s_k, float* s_v, float* s_q_test, hipStream_t s);
-// Quantize one (B,rows,H,D) tensor with per-(b,h) scales into (B,H,rows,D) codes.
-hipError_t launch_quantize_rows(int in_bf16, int B, int H, int D, int rows, const void* x,
-                                const float* scale, uint8_t* codes, hipStream_t s);
-// Quantize V (B,N,H,D) into the tile-transposed layout the FP8 kernel reads.
-hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, const void* v,
-                                   const float* scale, uint8_t* v8t, hipStream_t s);
+                       uint32_t* partial, hipStream_t s);
+// One launch quantizing every tensor whose input is non-NULL (Q_test only when M > 0)
+// with the per-(b,h) scales of the query-scale mode, s = fl32(amax/448) (1 where that is
+// 0), reduced from the slice maxima.  V goes to the tile layout v8t when it is non-NULL,
+// else to (B,H,N,D) v8.  Stores scales[4][B][H] (s_q, s_k, s_v, s_q_test) for the tensors
+// quantized (s_q_test with Q_train when there is no Q_test) and, when the pointers are
+// non-NULL, copies of them.
+hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, int N, int M,
+                           const void* q_train, const void* k, const void* v, const void* q_test,
+                           uint8_t* q8_train, uint8_t* k8, uint8_t* v8, uint8_t* v8t, uint8_t* q8_test,
+                           const uint32_t* partial, float* scales, float* s_q, float* s_k, float* s_v,
+                           float* s_q_test, hipStream_t s);
 // Re-lay (B,H,N,D) V codes into the tile-transposed layout.
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8,
                                    uint8_t* v8t, hipStream_t s);

@@ -2,22 +2,33 @@
 //
 // Eq. (2) of the paper (Sec. 3): s = max|X^(h)| / 448 per head,
 // X_8 = rn_fp8(clamp(X / s, -448, 448)), fp32 scale; test queries use the
-// train-query scale.  Three passes, all HBM-bound streams of the inputs:
-//   1. amax_kernel   -- per-(tensor, b, h) max|x| with 16-byte loads; the
-//                       maximum of non-negative floats is taken on their bit
-//                       patterns as uint32 (order-preserving, exact), first in
-//                       LDS, then one global atomic max per head per block;
-//   2. scales_kernel -- s = fl32(amax / 448) (IEEE division), 1 where 0;
-//   3. quantize_*    -- fl32(x / s) (IEEE division), clamp, and the hardware
-//                       fp32 -> e4m3fn conversion, which rounds to nearest
-//                       even; codes go to (B,H,rows,D), or, for V on the fused
-//                       path, to the tile-transposed layout of attn_fp8.hip.
+// train-query scale.  Two launches, both HBM-bound streams of the inputs:
+//   1. amax_kernel     -- one block per (row slice, tensor, table, head group)
+//                         takes max|x| per head with 16-byte loads (the maximum
+//                         of non-negative floats is taken on their bit patterns
+//                         as uint32: order-preserving and exact) and writes it to
+//                         its own slot of partial[tensor][b][h][slice].  Every
+//                         slot is written exactly once, so nothing has to be
+//                         zeroed first and no global atomics are needed;
+//   2. quantize_kernel -- one launch over all tensors (V, K, Q_train, Q_test,
+//                         in that order).  Each block first reduces the slice
+//                         maxima of the heads it covers to their scales,
+//                         s = fl32(amax / 448) (IEEE division, 1 where 0), then
+//                         writes fl32(x / s) (IEEE division), clamped, through
+//                         the hardware fp32 -> e4m3fn conversion (round to
+//                         nearest even) to (B,H,rows,D), or, for V on the fused
+//                         path, to the tile-transposed layout of attn_fp8.hip.
+//                         The first block of each (tensor, table, heads) also
+//                         stores the scales.
+// A third kernel re-lays V codes that are already quantized into the tile
+// layout (the prequantized entry point).
 #include "common.h"
 
 namespace tfm {
 namespace {
 
 constexpr int kThreads = 256;
+constexpr int kHeadGroup = 32;  // heads per block in the row kernels (their scales are kept in LDS)
 
 template <typename T> struct Vec;
 template <> struct Vec<float> { static constexpr int n = 4; };
@@ -65,110 +76,232 @@ __device__ inline uint32_t codes4(const float* x, float s) {
   return (uint32_t)w;
 }
 
-// Thread -> (row offset, vector position) map shared by the row kernels: a
-// row of H*D elements is `vpr` 16-byte vectors; with vpr <= 256 each thread
-// keeps one fixed position (so one fixed head) and strides over rows.
+// Thread -> (row offset, vector position) map of the row kernels for one block
+// of `hn` heads: a row of hn*D elements is `vpr` 16-byte vectors; with vpr <=
+// 256 each thread keeps one fixed position (so one fixed head) and strides over
+// rows.
 struct RowMap {
   int vpr, lanes_per_row, rows_per_iter;
-  __device__ RowMap(int H, int D, int vec) {
-    vpr = H * D / vec;
+  __device__ RowMap(int hn, int D, int vec) {
+    vpr = hn * D / vec;
     lanes_per_row = vpr < kThreads ? vpr : kThreads;
     rows_per_iter = kThreads / lanes_per_row;
   }
 };
 
+__host__ __device__ inline int head_groups(int H) { return (H + kHeadGroup - 1) / kHeadGroup; }
+
+struct AmaxArgs {
+  int first_tensor;       // tensors first_tensor .. first_tensor + gridDim.y / groups - 1
+  int B, H, D, N, M;
+  const void* x[4];       // Q_train, K, V, Q_test
+  uint32_t* partial;      // [4][B][H][kAmaxSlices]
+};
+
 template <typename T>
-__global__ __launch_bounds__(kThreads) void amax_kernel(int first_tensor, int B, int H, int D, int N, int M,
-                                                        int rows_per_chunk,
-                                                        const T* __restrict__ q, const T* __restrict__ k,
-                                                        const T* __restrict__ v, const T* __restrict__ qt,
-                                                        uint32_t* __restrict__ amax) {
-  extern __shared__ uint32_t smax[];  // H entries
+__global__ __launch_bounds__(kThreads) void amax_kernel(AmaxArgs a) {
+  __shared__ uint32_t smax[kHeadGroup];
   constexpr int VEC = Vec<T>::n;
-  const int tensor = first_tensor + blockIdx.y, b = blockIdx.z;
-  const T* x = tensor == 0 ? q : (tensor == 1 ? k : (tensor == 2 ? v : qt));
-  if (tensor == 3) N = M;   // the test queries have M rows
-  if ((int)blockIdx.x * rows_per_chunk >= N) return;
-  for (int i = threadIdx.x; i < H; i += kThreads) smax[i] = 0;
+  const int groups = head_groups(a.H);
+  const int tensor = a.first_tensor + blockIdx.y / groups;
+  const int h0 = (blockIdx.y % groups) * kHeadGroup, hn = min(kHeadGroup, a.H - h0);
+  const int b = blockIdx.z, g = blockIdx.x;
+  const int rows = tensor == 3 ? a.M : a.N;
+  if (g >= amax_slices(rows)) return;   // whole block: this tensor has fewer slices
+  const int H = a.H, D = a.D;
+  const int sr = amax_slice_rows(rows);
+  const int r0 = g * sr, r1 = min(rows, r0 + sr);
+  if (threadIdx.x < hn) smax[threadIdx.x] = 0;
   __syncthreads();
-  const RowMap rm(H, D, VEC);
+  const RowMap rm(hn, D, VEC);
   const int t = threadIdx.x;
-  const int r0 = blockIdx.x * rows_per_chunk;
-  const int r1 = min(N, r0 + rows_per_chunk);
   if (t < rm.rows_per_iter * rm.lanes_per_row) {
     const int rr = t / rm.lanes_per_row;
+    const T* x = (const T*)a.x[tensor] + ((size_t)b * rows) * H * D + (size_t)h0 * D;
+    const size_t step = (size_t)rm.rows_per_iter * H * D;
     for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
       uint32_t m = 0;
-      const T* base = x + ((size_t)b * N) * H * D + (size_t)p * VEC;
-      const size_t step = (size_t)rm.rows_per_iter * H * D;
-      int row = r0 + rr;
-      // four independent 16-byte loads in flight per thread, then the remainder
-      for (; row + 3 * rm.rows_per_iter < r1; row += 4 * rm.rows_per_iter) {
+      const T* base = x + (size_t)p * VEC;
+      // eight independent 16-byte loads in flight per thread; rows past the slice read as 0
+      for (int row = r0 + rr; row < r1; row += 8 * rm.rows_per_iter) {
         const T* src = base + (size_t)row * H * D;
-        const u32x4 w0 = *reinterpret_cast<const u32x4*>(src);
-        const u32x4 w1 = *reinterpret_cast<const u32x4*>(src + step);
-        const u32x4 w2 = *reinterpret_cast<const u32x4*>(src + 2 * step);
-        const u32x4 w3 = *reinterpret_cast<const u32x4*>(src + 3 * step);
-        m = max(max(m, absmax_bits(w0, (T*)nullptr)), absmax_bits(w1, (T*)nullptr));
-        m = max(max(m, absmax_bits(w2, (T*)nullptr)), absmax_bits(w3, (T*)nullptr));
-      }
-      for (; row < r1; row += rm.rows_per_iter) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(base + (size_t)row * H * D);
-        m = max(m, absmax_bits(w, (T*)nullptr));
+        u32x4 w[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          w[u] = row + u * rm.rows_per_iter < r1 ? *reinterpret_cast<const u32x4*>(src + u * step)
+                                                 : u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+        for (int u = 0; u < 8; ++u) m = max(m, absmax_bits(w[u], (T*)nullptr));
       }
       atomicMax(&smax[p * VEC / D], m);
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < H; i += kThreads)
-    if (smax[i]) atomicMax(&amax[((size_t)tensor * B + b) * H + i], smax[i]);
+  if (threadIdx.x < hn)
+    a.partial[(((size_t)tensor * a.B + b) * H + h0 + threadIdx.x) * kAmaxSlices + g] = smax[threadIdx.x];
 }
 
-__global__ void fill_zero_kernel(uint32_t* p, int n) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) p[i] = 0u;
+// ---- quantize: one launch over the code tensors of a call ----
+
+struct QSeg {
+  const void* x;    // (B, rows, H, D) input
+  uint8_t* codes;   // (B, H, rows, D) codes, or the V tile layout when v_tiles
+  float* s_out;     // caller's copy of this tensor's (B, H) scales, or NULL
+  int tensor;       // 0 Q_train, 1 K, 2 V, 3 Q_test (the amax and scale slot)
+  int v_tiles;      // 1: 64-key tiles in the transposed layout of attn_fp8.hip
+  int rows;         // N, or M for Q_test
+  int rpc;          // rows per block (row layout)
+  int per_table;    // blocks per table
+  int first;        // first block of the segment in the grid
+};
+
+struct QArgs {
+  QSeg seg[4];
+  int nseg;
+  int B, H, D, N, M, mode;
+  int train_q_sets_test_slot;  // the Q_train segment also stores slot 3 (no Q_test segment)
+  const uint32_t* partial;
+  float* scales;               // [4][B*H]: s_q, s_k, s_v, s_q_test
+  float* s_q_test_out;         // caller's copy of s_q_test, or NULL
+};
+
+// Max of the slice maxima of one (tensor, b, h), reduced by one wave; every lane returns it.
+__device__ inline uint32_t wave_head_amax(const QArgs& a, int tensor, int b, int h, int lane) {
+  const int n = amax_slices(tensor == 3 ? a.M : a.N);
+  const uint32_t* p = a.partial + (((size_t)tensor * a.B + b) * a.H + h) * kAmaxSlices;
+  uint32_t m = 0;
+  for (int g = lane; g < n; g += 64) m = max(m, p[g]);
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+  return m;
 }
 
-// s = fl32(amax / 448), 1 where that is 0.  scales[4][BH] = s_q (train), s_k, s_v,
-// s_q_test.  Query-scale modes: shared -> s_q_test = s_q; per call -> each from
-// its own rows; joint -> both from the max over train and test rows.
 __device__ inline float scale_of(uint32_t amax_bits) {
   float s = __uint_as_float(amax_bits) / 448.0f;
   return s == 0.0f ? 1.0f : s;
 }
-__global__ void scales_kernel(int BH, int q_scale_mode, const uint32_t* __restrict__ amax, float* __restrict__ scales,
-                              float* s_q, float* s_k, float* s_v, float* s_q_test) {
-  int i = blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= BH) return;
-  const uint32_t aq = amax[i], aqt = amax[3 * BH + i];
-  const float sq = scale_of(q_scale_mode == TFM_QSCALE_JOINT ? max(aq, aqt) : aq);
-  const float sqt = q_scale_mode == TFM_QSCALE_PER_CALL ? scale_of(aqt) : sq;
-  const float sk = scale_of(amax[BH + i]), sv = scale_of(amax[2 * BH + i]);
-  scales[i] = sq; scales[BH + i] = sk; scales[2 * BH + i] = sv; scales[3 * BH + i] = sqt;
-  if (s_q) s_q[i] = sq;
-  if (s_k) s_k[i] = sk;
-  if (s_v) s_v[i] = sv;
-  if (s_q_test) s_q_test[i] = sqt;
+
+// Scale of slot `tensor` for head (b, h) under the query-scale mode: shared ->
+// test queries on the train-query scale; per call -> each query set on its own
+// rows; joint -> both on the max over train and test rows.  The test-query
+// maxima exist only when the mode needs them and there are test rows.
+__device__ inline float wave_scale(const QArgs& a, int tensor, int b, int h, int lane) {
+  if (tensor == 1 || tensor == 2) return scale_of(wave_head_amax(a, tensor, b, h, lane));
+  const bool have_test = a.mode != TFM_QSCALE_SHARED && a.M > 0;
+  if (a.mode == TFM_QSCALE_PER_CALL && tensor == 3) return scale_of(have_test ? wave_head_amax(a, 3, b, h, lane) : 0u);
+  uint32_t m = wave_head_amax(a, 0, b, h, lane);
+  if (a.mode == TFM_QSCALE_JOINT && have_test) m = max(m, wave_head_amax(a, 3, b, h, lane));
+  return scale_of(m);
+}
+
+// Position of key kk (0..63) of a 64-key tile inside the tile-transposed V
+// layout: the PV product of attn_fp8.hip feeds lane half `hf` and byte j of
+// its B operand with key ((j%16)/4)*8 + hf*4 + j%4 + 32*(j/16) (the row
+// order of the QK^T accumulator), so V is stored in that order.
+__device__ inline int v_tile_pos(int kk) {
+  const int tile = kk >> 5, kp = kk & 31;
+  const int g = kp >> 3, hf = (kp >> 2) & 1, i = kp & 3;
+  return hf * 32 + tile * 16 + g * 4 + i;
 }
 
 template <typename T>
-__global__ __launch_bounds__(kThreads) void quantize_rows_kernel(int H, int D, int rows, int rows_per_chunk,
-                                                                 const T* __restrict__ x,
-                                                                 const float* __restrict__ scale,
-                                                                 uint8_t* __restrict__ codes) {
+__global__ __launch_bounds__(kThreads) void quantize_kernel(QArgs a) {
+  __shared__ float sc[kHeadGroup];
+  __shared__ uint8_t tile_codes[128 * 64];   // one 64-key V tile, transposed (D <= 128)
   constexpr int VEC = Vec<T>::n;
-  const int b = blockIdx.y;
-  const int r0 = blockIdx.x * rows_per_chunk;
-  const RowMap rm(H, D, VEC);
+  int si = 0;
+  while (si + 1 < a.nseg && (int)blockIdx.x >= a.seg[si + 1].first) ++si;
+  const QSeg& sg = a.seg[si];
+  const int local = blockIdx.x - sg.first;
+  const int b = local / sg.per_table, rem = local % sg.per_table;
+  const int H = a.H, D = a.D, rows = sg.rows;
+  const int wave = threadIdx.x / 64, lane = threadIdx.x % 64;
+
+  if (sg.v_tiles) {
+    // one block per (b, h, 64-key tile) of V
+    const int ntiles = (rows + 63) / 64;
+    const int h = rem / ntiles, kt = rem % ntiles;
+    if (wave == 0) {
+      const float s = wave_scale(a, sg.tensor, b, h, lane);
+      if (lane == 0) {
+        sc[0] = s;
+        if (kt == 0) {
+          a.scales[(size_t)sg.tensor * a.B * H + b * H + h] = s;
+          if (sg.s_out) sg.s_out[b * H + h] = s;
+        }
+      }
+    }
+    __syncthreads();
+    const float s = sc[0];
+    const int per_row = D / VEC;
+    const int items = 64 * per_row;       // a multiple of 2 * 256 for D = 64 and 128
+    constexpr int U = 2;
+    for (int i0 = threadIdx.x; i0 < items; i0 += U * kThreads) {
+      u32x4 w[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {       // loads first
+        const int i = i0 + u * kThreads;
+        const int key = kt * 64 + i / per_row;
+        w[u] = (i < items && key < rows)
+                   ? *reinterpret_cast<const u32x4*>((const T*)sg.x + (((size_t)b * rows + key) * H + h) * D +
+                                                     (i % per_row) * VEC)
+                   : u32x4{0u, 0u, 0u, 0u};
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int i = i0 + u * kThreads;
+        if (i >= items) break;
+        const int kk = i / per_row, c = i % per_row;
+        uint32_t cw[VEC / 4];
+        float xv[VEC];
+        unpack(w[u], xv, (T*)nullptr);
+#pragma unroll
+        for (int j = 0; j < VEC / 4; ++j) cw[j] = codes4(xv + 4 * j, s);   // zero inputs give code 0
+        const int pos = v_tile_pos(kk);
+#pragma unroll
+        for (int j = 0; j < VEC; ++j) tile_codes[(c * VEC + j) * 64 + pos] = (uint8_t)(cw[j / 4] >> (8 * (j % 4)));
+      }
+    }
+    __syncthreads();
+    uint8_t* dst = sg.codes + (((size_t)b * H + h) * ntiles + kt) * D * 64;
+    for (int i = threadIdx.x; i < D * 4; i += kThreads)
+      reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(tile_codes)[i];
+    return;
+  }
+
+  // row layout: one block per (b, row chunk, head group)
+  const int groups = head_groups(H);
+  const int chunk = rem / groups;
+  const int h0 = (rem % groups) * kHeadGroup, hn = min(kHeadGroup, H - h0);
+  const bool store = chunk == 0;
+  const bool store_test = store && sg.tensor == 0 && a.train_q_sets_test_slot;
+  for (int j = wave; j < hn; j += kThreads / 64) {
+    const float s = wave_scale(a, sg.tensor, b, h0 + j, lane);
+    const float st = store_test ? wave_scale(a, 3, b, h0 + j, lane) : 0.0f;
+    if (lane == 0) {
+      sc[j] = s;
+      if (store) {
+        const size_t bh = (size_t)b * H + h0 + j;
+        a.scales[(size_t)sg.tensor * a.B * H + bh] = s;
+        if (sg.s_out) sg.s_out[bh] = s;
+        if (store_test) {
+          a.scales[(size_t)3 * a.B * H + bh] = st;
+          if (a.s_q_test_out) a.s_q_test_out[bh] = st;
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const RowMap rm(hn, D, VEC);
   const int t = threadIdx.x;
-  const int r1 = min(rows, r0 + rows_per_chunk);
+  const int r0 = chunk * sg.rpc, r1 = min(rows, r0 + sg.rpc);
   if (t >= rm.rows_per_iter * rm.lanes_per_row) return;
   const int rr = t / rm.lanes_per_row;
   for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
-    const int h = p * VEC / D, d0 = (p * VEC) % D;
-    const float s = scale[b * H + h];
-    const T* src = x + ((size_t)b * rows) * H * D + (size_t)p * VEC;
-    uint8_t* dst = codes + (((size_t)b * H + h) * rows) * D + d0;
+    const int hl = p * VEC / D, d0 = (p * VEC) % D;
+    const float s = sc[hl];
+    const T* src = (const T*)sg.x + ((size_t)b * rows) * H * D + (size_t)h0 * D + (size_t)p * VEC;
+    uint8_t* dst = sg.codes + (((size_t)b * H + h0 + hl) * rows) * D + d0;
     // U rows per thread-iteration: their loads are all issued before any is converted
     constexpr int U = 4;
     int row = r0 + rr;
@@ -198,70 +331,22 @@ __global__ __launch_bounds__(kThreads) void quantize_rows_kernel(int H, int D, i
   }
 }
 
-// Position of key kk (0..63) of a 64-key tile inside the tile-transposed V
-// layout: the PV product of attn_fp8.hip feeds lane half `hf` and byte j of
-// its B operand with key ((j%16)/4)*8 + hf*4 + j%4 + 32*(j/16) (the row
-// order of the QK^T accumulator), so V is stored in that order.
-__device__ inline int v_tile_pos(int kk) {
-  const int tile = kk >> 5, kp = kk & 31;
-  const int g = kp >> 3, hf = (kp >> 2) & 1, i = kp & 3;
-  return hf * 32 + tile * 16 + g * 4 + i;
-}
-
-// One block per (b*H + h, 64-key tile): codes of the tile's V rows (from
-// inputs or from (B,H,N,D) codes) transposed through LDS into
-// v8t[((b*H + h)*ntiles + tile)*D*64 + d*64 + pos].  Keys >= N get code 0.
-template <typename T, bool FROM_CODES>
-__global__ __launch_bounds__(kThreads) void v_tiles_kernel(int H, int D, int N, const T* __restrict__ src,
-                                                           const float* __restrict__ scale,
-                                                           uint8_t* __restrict__ v8t) {
+// One block per (b*H + h, 64-key tile): (B,H,N,D) codes transposed through LDS
+// into v8t[((b*H + h)*ntiles + tile)*D*64 + d*64 + pos].  Keys >= N get code 0.
+__global__ __launch_bounds__(kThreads) void relayout_v_tiles_kernel(int D, int N, const uint8_t* __restrict__ src,
+                                                                    uint8_t* __restrict__ v8t) {
   __shared__ uint8_t tile_codes[128 * 64];
   const int bh = blockIdx.y, kt = blockIdx.x;
-  const int b = bh / H, h = bh % H;
   const int ntiles = (N + 63) / 64;
-  if constexpr (FROM_CODES) {
-    // src: (B,H,N,D) codes; 16 codes per thread-iteration
-    const int per_row = D / 16;
-    for (int i = threadIdx.x; i < 64 * per_row; i += kThreads) {
-      const int kk = i / per_row, c = i % per_row;
-      const int key = kt * 64 + kk;
-      u32x4 w = {0u, 0u, 0u, 0u};
-      if (key < N) w = *reinterpret_cast<const u32x4*>(src + ((size_t)bh * N + key) * D + c * 16);
-      const int pos = v_tile_pos(kk);
+  const int per_row = D / 16;   // 16 codes per thread-iteration
+  for (int i = threadIdx.x; i < 64 * per_row; i += kThreads) {
+    const int kk = i / per_row, c = i % per_row;
+    const int key = kt * 64 + kk;
+    u32x4 w = {0u, 0u, 0u, 0u};
+    if (key < N) w = *reinterpret_cast<const u32x4*>(src + ((size_t)bh * N + key) * D + c * 16);
+    const int pos = v_tile_pos(kk);
 #pragma unroll
-      for (int j = 0; j < 16; ++j) tile_codes[(c * 16 + j) * 64 + pos] = (uint8_t)(w[j / 4] >> (8 * (j % 4)));
-    }
-  } else {
-    constexpr int VEC = Vec<T>::n;
-    const float s = scale[bh];
-    const int per_row = D / VEC;
-    const int items = 64 * per_row;       // a multiple of 2 * 256 for D = 64 and 128
-    constexpr int U = 2;
-    for (int i0 = threadIdx.x; i0 < items; i0 += U * kThreads) {
-      u32x4 w[U];
-#pragma unroll
-      for (int u = 0; u < U; ++u) {       // loads first
-        const int i = i0 + u * kThreads;
-        const int key = kt * 64 + i / per_row;
-        w[u] = (i < items && key < N)
-                   ? *reinterpret_cast<const u32x4*>(src + (((size_t)b * N + key) * H + h) * D + (i % per_row) * VEC)
-                   : u32x4{0u, 0u, 0u, 0u};
-      }
-#pragma unroll
-      for (int u = 0; u < U; ++u) {
-        const int i = i0 + u * kThreads;
-        if (i >= items) break;
-        const int kk = i / per_row, c = i % per_row;
-        uint32_t cw[VEC / 4];
-        float xv[VEC];
-        unpack(w[u], xv, (T*)nullptr);
-#pragma unroll
-        for (int j = 0; j < VEC / 4; ++j) cw[j] = codes4(xv + 4 * j, s);   // zero inputs give code 0
-        const int pos = v_tile_pos(kk);
-#pragma unroll
-        for (int j = 0; j < VEC; ++j) tile_codes[(c * VEC + j) * 64 + pos] = (uint8_t)(cw[j / 4] >> (8 * (j % 4)));
-      }
-    }
+    for (int j = 0; j < 16; ++j) tile_codes[(c * 16 + j) * 64 + pos] = (uint8_t)(w[j / 4] >> (8 * (j % 4)));
   }
   __syncthreads();
   uint8_t* dst = v8t + ((size_t)bh * ntiles + kt) * D * 64;
@@ -269,13 +354,18 @@ __global__ __launch_bounds__(kThreads) void v_tiles_kernel(int H, int D, int N, 
     reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(tile_codes)[i];
 }
 
-int chunk_rows(int rows, int H, int D, int esize) {
-  // about 64 KiB of input per block (measured best among 64 KiB .. 512 KiB)
-  long per_row = (long)H * D * esize;
+// Rows per quantize block: about 64 KiB of input (measured best among 64 KiB .. 512 KiB).
+int chunk_rows(int rows, int hn, int D, int esize) {
+  long per_row = (long)hn * D * esize;
   long r = (65536 + per_row - 1) / per_row;
   if (r < 1) r = 1;
   if (r > rows) r = rows > 0 ? rows : 1;
   return (int)r;
+}
+
+__global__ void fill_zero_kernel(uint32_t* p, int n) {
+  int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) p[i] = 0u;
 }
 
 }  // namespace
@@ -287,62 +377,61 @@ hipError_t launch_fill_zero_u32(uint32_t* p, int n, hipStream_t s) {
 }
 
 hipError_t launch_amax(int in_bf16, int first, int last, int B, int H, int D, int N, int M, const void* q_train,
-                       const void* k, const void* v, const void* q_test, uint32_t* amax, hipStream_t s) {
+                       const void* k, const void* v, const void* q_test, uint32_t* partial, hipStream_t s) {
   if (last == 3 && M == 0) last = 2;   // no test rows to scan
   if (last < first) return hipSuccess;
+  AmaxArgs a;
+  a.first_tensor = first;
+  a.B = B; a.H = H; a.D = D; a.N = N; a.M = M;
+  a.x[0] = q_train; a.x[1] = k; a.x[2] = v; a.x[3] = q_test;
+  a.partial = partial;
+  int slices = 0;
+  for (int t = first; t <= last; ++t) slices = max(slices, amax_slices(t == 3 ? M : N));
+  dim3 grid(slices, (last - first + 1) * head_groups(H), B);
+  if (in_bf16) hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), 0, s, a);
+  else hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, int N, int M, const void* q_train,
+                           const void* k, const void* v, const void* q_test, uint8_t* q8_train, uint8_t* k8,
+                           uint8_t* v8, uint8_t* v8t, uint8_t* q8_test, const uint32_t* partial, float* scales,
+                           float* s_q, float* s_k, float* s_v, float* s_q_test, hipStream_t s) {
+  QArgs a;
+  a.B = B; a.H = H; a.D = D; a.N = N; a.M = M; a.mode = q_scale_mode;
+  a.partial = partial; a.scales = scales; a.s_q_test_out = s_q_test;
   const int esize = in_bf16 ? 2 : 4;
-  const int rows = first == 3 ? M : ((last == 3 && M > N) ? M : N);   // the most rows of any launched tensor
-  const int rpc = chunk_rows(first == 3 ? M : N, H, D, esize);
-  dim3 grid((rows + rpc - 1) / rpc, last - first + 1, B);
-  size_t lds = (size_t)H * sizeof(uint32_t);
-  if (in_bf16)
-    hipLaunchKernelGGL(amax_kernel<uint16_t>, grid, dim3(kThreads), lds, s, first, B, H, D, N, M, rpc,
-                       (const uint16_t*)q_train, (const uint16_t*)k, (const uint16_t*)v, (const uint16_t*)q_test,
-                       amax);
-  else
-    hipLaunchKernelGGL(amax_kernel<float>, grid, dim3(kThreads), lds, s, first, B, H, D, N, M, rpc,
-                       (const float*)q_train, (const float*)k, (const float*)v, (const float*)q_test, amax);
-  return hipGetLastError();
-}
-
-hipError_t launch_scales(int BH, int q_scale_mode, const uint32_t* amax, float* scales, float* s_q, float* s_k,
-                         float* s_v, float* s_q_test, hipStream_t s) {
-  hipLaunchKernelGGL(scales_kernel, dim3((BH + 255) / 256), dim3(256), 0, s, BH, q_scale_mode, amax, scales, s_q,
-                     s_k, s_v, s_q_test);
-  return hipGetLastError();
-}
-
-hipError_t launch_quantize_rows(int in_bf16, int B, int H, int D, int rows, const void* x, const float* scale,
-                                uint8_t* codes, hipStream_t s) {
-  if (rows <= 0) return hipSuccess;
-  const int esize = in_bf16 ? 2 : 4;
-  const int rpc = chunk_rows(rows, H, D, esize);
-  dim3 grid((rows + rpc - 1) / rpc, B);
-  if (in_bf16)
-    hipLaunchKernelGGL(quantize_rows_kernel<uint16_t>, grid, dim3(kThreads), 0, s, H, D, rows, rpc,
-                       (const uint16_t*)x, scale, codes);
-  else
-    hipLaunchKernelGGL(quantize_rows_kernel<float>, grid, dim3(kThreads), 0, s, H, D, rows, rpc,
-                       (const float*)x, scale, codes);
-  return hipGetLastError();
-}
-
-hipError_t launch_quantize_v_tiles(int in_bf16, int B, int H, int D, int N, const void* v, const float* scale,
-                                   uint8_t* v8t, hipStream_t s) {
-  dim3 grid((N + 63) / 64, B * H);
-  if (in_bf16)
-    hipLaunchKernelGGL((v_tiles_kernel<uint16_t, false>), grid, dim3(kThreads), 0, s, H, D, N,
-                       (const uint16_t*)v, scale, v8t);
-  else
-    hipLaunchKernelGGL((v_tiles_kernel<float, false>), grid, dim3(kThreads), 0, s, H, D, N, (const float*)v,
-                       scale, v8t);
+  const int groups = head_groups(H);
+  const int hn = H < kHeadGroup ? H : kHeadGroup;
+  long total = 0;
+  a.nseg = 0;
+  auto add = [&](const void* x, uint8_t* codes, float* s_out, int tensor, int v_tiles, int rows) {
+    if (!x || rows <= 0) return;
+    QSeg& g = a.seg[a.nseg++];
+    g.x = x; g.codes = codes; g.s_out = s_out; g.tensor = tensor; g.v_tiles = v_tiles; g.rows = rows;
+    g.rpc = chunk_rows(rows, hn, D, esize);
+    g.per_table = v_tiles ? H * ((rows + 63) / 64) : ((rows + g.rpc - 1) / g.rpc) * groups;
+    g.first = (int)total;
+    total += (long)B * g.per_table;
+  };
+  // V, K, then the queries: the reverse of the order the amax pass reads them in, so the
+  // second read of the most recently scanned tensors can still hit the memory-side cache
+  add(v, v8t ? v8t : v8, s_v, 2, v8t != nullptr, N);
+  add(k, k8, s_k, 1, 0, N);
+  add(q_train, q8_train, s_q, 0, 0, N);
+  add(q_test, q8_test, nullptr, 3, 0, M);
+  a.train_q_sets_test_slot = !(q_test && M > 0);
+  if (a.nseg > 0 && a.seg[a.nseg - 1].tensor == 3) a.seg[a.nseg - 1].s_out = s_q_test;
+  if (total == 0) return hipSuccess;
+  if (total > INT32_MAX) return hipErrorInvalidValue;
+  if (in_bf16) hipLaunchKernelGGL(quantize_kernel<uint16_t>, dim3((unsigned)total), dim3(kThreads), 0, s, a);
+  else hipLaunchKernelGGL(quantize_kernel<float>, dim3((unsigned)total), dim3(kThreads), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8, uint8_t* v8t, hipStream_t s) {
   dim3 grid((N + 63) / 64, B * H);
-  hipLaunchKernelGGL((v_tiles_kernel<uint8_t, true>), grid, dim3(kThreads), 0, s, H, D, N, v8,
-                     (const float*)nullptr, v8t);
+  hipLaunchKernelGGL(relayout_v_tiles_kernel, grid, dim3(kThreads), 0, s, D, N, v8, v8t);
   return hipGetLastError();
 }
 

@@ -39,14 +39,16 @@ def test_block_kv_and_workspace_queries():
     assert tfm.tfm_icl_attention_fp8_block_kv(64) == 128
     assert tfm.tfm_icl_attention_fp8_block_kv(128) == 128
     assert tfm.tfm_icl_attention_fp8_block_kv(96) == 0
-    assert tfm.tfm_quantize_workspace_bytes(2, 6) == 512
+    # the slice maxima of the amax pass (4 tensors x B*H heads x 128 slices, uint32) and the
+    # scales (4*B*H floats), each 256-aligned
+    assert tfm.tfm_quantize_workspace_bytes(2, 6) == 4 * 12 * 128 * 4 + 256
     assert tfm.tfm_quantize_workspace_bytes(0, 6) == 0
-    # amax and scales (4*B*H words each, 256-aligned), codes of Q_train, Q_test, K (N or M x D per head),
-    # V tiles (ceil(N/64)*64*D)
+    assert tfm.tfm_quantize_workspace_bytes(1, 65536) == 0
+    # slice maxima and scales, codes of Q_train, Q_test, K (N or M x D per head), V tiles (ceil(N/64)*64*D)
     B, H, D, N, M = 2, 6, 64, 65536, 16384
-    want = 256 + 256 + B * H * (N * D + M * D + N * D + N * D)
+    want = 4 * B * H * 128 * 4 + 256 + B * H * (N * D + M * D + N * D + N * D)
     assert tfm.tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M) == want
-    assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 64, 65, 0) >= 256 * 2 + 65 * 64 * 2 + 128 * 64
+    assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 64, 65, 0) >= 2048 + 256 + 65 * 64 * 2 + 128 * 64
     assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 96, 10, 0) == 0
     assert tfm.tfm_icl_attention_fp8_prequantized_workspace_bytes(1, 2, 128, 100) == 2 * 128 * 128
 
