@@ -145,3 +145,34 @@ def test_gate_passes_the_options_to_either_path(N, expect_fp8):
     else:
         d = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha, test_kv_heads=1)
     assert torch.equal(o_tr, d[0]) and torch.equal(o_te, d[1])
+
+
+@pytest.mark.parametrize("mode", MODES)
+def test_many_heads_and_row_slices(mode):
+    # 34 heads: the quantize kernels take at most 32 heads per block, so every row splits
+    # over two blocks; 1300 train rows: the amax pass keeps 82 slice maxima of 16 rows per
+    # head, the last slice ragged.  Codes and scales bit-exact (Eq. (2)); the fused quantize
+    # path (V into the kernel's tile layout, scales reduced inside the quantize launch)
+    # bitwise equal to attention on the public codes; both within T1' of the kernel model.
+    w = Workload("wide", B=2, H=34, D=64, N=1300, M=300, dtype="bf16", seed=52)
+    x = skewed_inputs(w, 53)
+    g = gpu_inputs(x, torch.bfloat16)
+    xr = {k: torch.from_numpy(v).to(torch.bfloat16).float().numpy() for k, v in x.items()}
+    ref = OQ.quantize_qkv_per_head(xr["q_train"], xr["k"], xr["v"], xr["q_test"], q_scale_mode=mode)
+    q = tfm.tfm_quantize_qkv_per_head(g["q_train"], g["k"], g["v"], g["q_test"], q_scale_mode=mode)
+    for k in CODE_KEYS + SCALE_KEYS:
+        assert np.array_equal(q[k].cpu().numpy(), ref[k]), (mode, k)
+    ws = tfm.tfm_icl_attention_fp8_quantize(g["q_train"], g["k"], g["v"], g["q_test"], q_scale_mode=mode)
+    a_tr, a_te = tfm.tfm_icl_attention_fp8_attend(ws, w.B, w.H, w.D, w.N, w.M, alpha=w.alpha)
+    p_tr, p_te = tfm.tfm_icl_attention_fp8_prequantized(q["q8_train"], q["k8"], q["v8"], q["q8_test"], q["s_q"],
+                                                        q["s_k"], q["s_v"], alpha=w.alpha, s_q_test=q["s_q_test"])
+    assert torch.equal(a_tr, p_tr) and torch.equal(a_te, p_te), mode
+    rt, re = sample_rows(w.N, 32, 54), sample_rows(w.M, 16, 55)
+    heads = [0, 31, 32, 33]     # both sides of the head-group boundary
+    sub = {k: v[:, heads] for k, v in ref.items()}   # codes (B,H,rows,D) and scales (B,H)
+    r_tr, r_te = OA.icl_attention_fp8_kernel_model(sub, w.alpha, BKV, rt, re)
+    a_tr, a_te = a_tr.cpu().numpy(), a_te.cpu().numpy()
+    for b in range(w.B):
+        for j, h in enumerate(heads):
+            assert_t1p(a_tr[b, rt, h], r_tr[b, :, j], ("train", mode, b, h))
+            assert_t1p(a_te[b, re, h], r_te[b, :, j], ("test", mode, b, h))
