@@ -193,8 +193,8 @@ int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int
  * depend on its batch, so the train-side state can be kept.
  *
  * fit: Eq. (2) for Q_train, K and V, then the train-train call into o_train.
- *   The workspace keeps the quantized train state (scales, Q_train, K, V
- *   codes) for later predict calls; size it with
+ *   The workspace keeps the quantized train state (the per-head absmax
+ *   partials, scales, Q_train, K, V codes) for later predict calls; size it with
  *   tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M_max) for the largest
  *   test batch M_max to come (M_max = 0 if none).
  * predict: Q_test (B, M, H, D) quantized with the train-query scale (or, with
