@@ -1,11 +1,13 @@
-"""HIP graph capture of the library's entry points.
+"""Execution models of the library's entry points: HIP graphs and concurrent streams.
 
 The library never allocates and enqueues only kernels (no memset or copy nodes),
 so a caller can capture a call into a HIP graph, for example the predict step of
 a serving loop, and replay it.  Every replay must equal the eager call on the
 same buffers bit for bit, with eager work of the program between replays, and a
 replay must follow inputs changed in place (the graph reads the same addresses).
-The eager calls are checked against the oracle in the other GPU tests."""
+It keeps no state outside the caller's buffers, so calls on different streams
+with their own workspaces may run concurrently.  The eager calls are checked
+against the oracle in the other GPU tests."""
 import pytest
 import torch
 
@@ -74,3 +76,26 @@ def test_fit_once_predict_replays_follow_new_test_batches():
         # and the same rows through the fused entry point (same fit state, same scales)
         _, f_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], batch, alpha=w.alpha)
         assert torch.equal(o_static, f_te), rep
+
+
+def test_two_streams_with_their_own_workspaces_match_sequential_calls():
+    # No state outside the caller's buffers: the same calls enqueued on two streams at once,
+    # each with its own workspace and outputs, give the sequential results bit for bit.
+    ws_args = []
+    for seed in (73, 74):
+        w = Workload("streams", B=1, H=4, D=64, N=5000, M=600, dtype="bf16", seed=seed)
+        ws_args.append((w, gpu_inputs(generate(w), torch.bfloat16)))
+    want = [tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+            for w, g in ws_args]
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    for s in streams:
+        s.wait_stream(torch.cuda.current_stream())
+    got = [None, None]
+    for rep in range(3):
+        for i, ((w, g), s) in enumerate(zip(ws_args, streams)):
+            with torch.cuda.stream(s):
+                got[i] = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+        torch.cuda.synchronize()
+        for i in range(2):
+            assert torch.equal(got[i][0], want[i][0]) and torch.equal(got[i][1], want[i][1]), (rep, i)
