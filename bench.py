@@ -263,7 +263,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print("bench.py measures one GPU only: the FP8 ICL attention of each (table, head) is independent, "
-              "and multi-GPU runs are not part of this build (asked for --gpus %d)" % args.gpus, file=sys.stderr)
+              "and the library has no multi-GPU path (asked for --gpus %d)" % args.gpus, file=sys.stderr)
         sys.exit(2)
 
     import numpy as np
