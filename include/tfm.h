@@ -35,8 +35,10 @@
  *    is returned.  TFM_ERR_HIP means the HIP runtime refused a launch; the
  *    launches of the same call before it may already be enqueued, so the
  *    outputs are then unspecified.  No C++ exception crosses this interface.
- *  - Inputs must be finite; for non-finite inputs the results are
- *    unspecified.
+ *  - Inputs must be finite, and so must the logits they produce in fp32:
+ *    alpha * q.k, and for the FP8 path the factor alpha * s_q * s_k * log2(e)
+ *    (it overflows only for activations beyond about 1e19 in both Q and K).
+ *    Otherwise the results are unspecified.
  */
 #ifndef TFM_H_
 #define TFM_H_
