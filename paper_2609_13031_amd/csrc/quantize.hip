@@ -6,10 +6,12 @@
 //   1. amax_kernel     -- one block per (row slice, tensor, table, head group)
 //                         takes max|x| per head with 16-byte loads (the maximum
 //                         of non-negative floats is taken on their bit patterns
-//                         as uint32: order-preserving and exact) and writes it to
-//                         its own slot of partial[tensor][b][h][slice].  Every
-//                         slot is written exactly once, so nothing has to be
-//                         zeroed first and no global atomics are needed;
+//                         as uint32: order-preserving and exact), reduces the
+//                         lanes of each head with cross-lane shuffles and the
+//                         block's lanes in LDS, and writes the result to its own
+//                         slot of partial[tensor][b][h][slice].  Every slot is
+//                         written exactly once, so nothing has to be zeroed
+//                         first and no global atomics are needed;
 //   2. quantize_kernel -- one launch over all tensors (V, K, Q_train, Q_test,
 //                         in that order).  Each block first reduces the slice
 //                         maxima of the heads it covers to their scales,
@@ -115,12 +117,20 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(AmaxArgs a) {
   __syncthreads();
   const RowMap rm(hn, D, VEC);
   const int t = threadIdx.x;
-  if (t < rm.rows_per_iter * rm.lanes_per_row) {
-    const int rr = t / rm.lanes_per_row;
-    const T* x = (const T*)a.x[tensor] + ((size_t)b * rows) * H * D + (size_t)h0 * D;
-    const size_t step = (size_t)rm.rows_per_iter * H * D;
-    for (int p = t % rm.lanes_per_row; p < rm.vpr; p += rm.lanes_per_row) {
-      uint32_t m = 0;
+  const int active = rm.rows_per_iter * rm.lanes_per_row;
+  const int rr = t / rm.lanes_per_row;
+  const T* x = (const T*)a.x[tensor] + ((size_t)b * rows) * H * D + (size_t)h0 * D;
+  const size_t step = (size_t)rm.rows_per_iter * H * D;
+  // The D / VEC lanes that hold one head's columns of one row slot are consecutive and
+  // aligned (lanes_per_row and the position stride are multiples of D / VEC, which
+  // divides 64), so they never straddle a wave.  Every thread runs the same number of
+  // position rounds, so the shuffles below always see the whole wave.
+  const int seg = D / VEC;
+  for (int p0 = 0; p0 < rm.vpr; p0 += rm.lanes_per_row) {
+    const int p = p0 + t % rm.lanes_per_row;
+    const bool mine = t < active && p < rm.vpr;
+    uint32_t m = 0;
+    if (mine) {
       const T* base = x + (size_t)p * VEC;
       // eight independent 16-byte loads in flight per thread; rows past the slice read as 0
       for (int row = r0 + rr; row < r1; row += 8 * rm.rows_per_iter) {
@@ -133,8 +143,11 @@ __global__ __launch_bounds__(kThreads) void amax_kernel(AmaxArgs a) {
 #pragma unroll
         for (int u = 0; u < 8; ++u) m = max(m, absmax_bits(w[u], (T*)nullptr));
       }
-      atomicMax(&smax[p * VEC / D], m);
     }
+    // the head's lanes combine their maxima with cross-lane shuffles; the first of them
+    // folds the result into the block's per-head maximum
+    for (int off = 1; off < seg; off <<= 1) m = max(m, (uint32_t)__shfl_xor((int)m, off, 64));
+    if (mine && t % seg == 0) atomicMax(&smax[p / seg], m);
   }
   __syncthreads();
   if (threadIdx.x < hn)
