@@ -28,10 +28,16 @@ T1_MAX, T1_RELF, T1_OUTLIER, T1_OUTLIER_FRAC = 1e-2, 1e-4, 2e-3, 1e-3   # report
 # the first with a 2x margin, EPS_ACC the second per key tile.
 EPS_DOT = 2.0 ** -11
 EPS_ACC = 2.0 ** -22
-# T1' -- on general inputs the FP8 path stays within relF 1e-2 of O_qp (the
-# accumulator noise above gives ~1e-3; a dropped key tile or a missing rescale
-# gives 0.17 and more), and elementwise within T2' of O_q.
-T1P_RELF = 1e-2
+# T1' -- on general inputs the FP8 path stays within relF 3e-2 of O_qp, and
+# elementwise within T2' of O_q.  The dot-product error above usually gives
+# ~1e-3.  It gives more on heads whose logits are both huge and sharp:
+# outlier channels in Q and in K push sum |q_k k_k| to 2e5 on one head of a
+# random-shape case (B=3, H=7, N=337, bf16, seed 1004), where 2^-11 of it is
+# 0.8 log2 units of logit and the rows span hundreds; the kernel is at relF
+# 1.1e-2 there, an emulated truncation of the products to 15 bits of the largest
+# moves O_qp by 1.4e-2, and T2' holds on every row.  A dropped key tile or a
+# missing rescale gives 0.17 and more.
+T1P_RELF = 3e-2
 
 
 def t1_metrics(got, ref):

@@ -1,0 +1,65 @@
+"""Seeded random shapes, dtypes and options through the fused FP8 path.
+
+Each case draws B, H, D, N, M, the input dtype, the query-scale mode and the
+grouped test K/V heads from a fixed generator, with inputs drawn like the
+workloads (per-head multipliers, outlier channels).  The codes and scales must
+equal the oracle's quantizer (Eq. (2)) bit for bit; every output row must be
+within T1' of the oracle's kernel model and a sample of rows within T2' of
+Eq. (1) on the dequantized inputs."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as OA
+from oracle import quantize as OQ
+from paper_2609_13031_amd import tfm
+from paper_2609_13031_amd.workloads import Workload, generate
+from parity import assert_t1p, assert_t2, gpu_inputs
+
+pytestmark = pytest.mark.gpu
+MODES = ("shared", "per_call", "joint")
+
+
+def draw_cases(n, seed):
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        H = int(rng.integers(1, 10))
+        divisors = [g for g in range(1, H + 1) if H % g == 0]
+        cases.append(dict(B=int(rng.integers(1, 4)), H=H, D=int(rng.choice([64, 128])),
+                          N=int(rng.integers(1, 700)), M=0 if rng.random() < 0.25 else int(rng.integers(1, 300)),
+                          dtype=str(rng.choice(["f32", "bf16"])), mode=str(rng.choice(MODES)),
+                          G=int(rng.choice(divisors)), seed=1000 + i))
+    return cases
+
+
+@pytest.mark.parametrize("case", draw_cases(24, 80), ids=lambda c: "B%(B)dH%(H)dD%(D)dN%(N)dM%(M)d-%(dtype)s-%(mode)s-G%(G)d" % c)
+def test_random_case(case):
+    c = case
+    w = Workload("random", B=c["B"], H=c["H"], D=c["D"], N=c["N"], M=c["M"], dtype=c["dtype"], seed=c["seed"])
+    x = generate(w)
+    tdt = torch.float32 if c["dtype"] == "f32" else torch.bfloat16
+    g = gpu_inputs(x, tdt)
+    q_test = g["q_test"] if c["M"] else None
+    q = tfm.tfm_quantize_qkv_per_head(g["q_train"], g["k"], g["v"], q_test, q_scale_mode=c["mode"])
+    o_tr, o_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], q_test, alpha=w.alpha,
+                                           q_scale_mode=c["mode"], test_kv_heads=c["G"])
+    torch.cuda.synchronize()
+    ref = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"] if c["M"] else None,
+                                   q_scale_mode=c["mode"])
+    keys = ["q8_train", "k8", "v8", "s_q", "s_k", "s_v", "s_q_test"] + (["q8_test"] if c["M"] else [])
+    for k in keys:
+        assert np.array_equal(q[k].cpu().numpy(), ref[k]), (c, k)
+    r_tr, r_te = OA.icl_attention_fp8_kernel_model(ref, w.alpha, tfm.tfm_icl_attention_fp8_block_kv(w.D),
+                                                   test_kv_heads=c["G"])
+    o_tr, o_te = o_tr.cpu().numpy(), o_te.cpu().numpy()
+    rows_t2 = np.unique(np.array([0, w.N // 2, w.N - 1]))
+    for b in range(w.B):
+        for h in range(w.H):
+            assert_t1p(o_tr[b, :, h], r_tr[b, :, h], (c, "train", b, h))
+            assert_t2(o_tr[b, rows_t2, h], ref, w.alpha, b, h, ref["q8_train"][b, h, rows_t2])
+            if c["M"]:
+                hk = OA.grouped_kv_head(h, w.H, c["G"])
+                assert_t1p(o_te[b, :, h], r_te[b, :, h], (c, "test", b, h))
+                assert_t2(o_te[b, :2, h], ref, w.alpha, b, h, ref["q8_test"][b, h, :2], s_query=ref["s_q_test"][b, h],
+                          hk=hk)
