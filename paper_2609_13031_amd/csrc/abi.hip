@@ -18,7 +18,7 @@ Fp8Workspace fp8_workspace_layout(int B, int H, int D, int N, int M) {
   Fp8Workspace w;
   const size_t bh = (size_t)B * H;
   size_t off = 0;
-  w.amax = off;      off += align256(amax_partial_words(B, H) * sizeof(uint32_t));
+  w.partial = off;   off += align256(amax_partial_words(B, H) * sizeof(uint32_t));
   w.scales = off;    off += align256(4 * bh * sizeof(float));
   w.q8_train = off;  off += align256(bh * N * D);
   w.k8 = off;        off += align256(bh * N * D);
@@ -145,10 +145,10 @@ int tfm_quantize_qkv_per_head(int in_dtype, const tfm_icl_options* opts, int B, 
   if (s_q_test && !aligned16(s_q_test)) return TFM_ERR_MISALIGNED;
   if (workspace_bytes < tfm_quantize_workspace_bytes(B, H)) return TFM_ERR_WORKSPACE_TOO_SMALL;
   uint8_t* ws = (uint8_t*)workspace;
-  uint32_t* amax = (uint32_t*)ws;
+  uint32_t* partial = (uint32_t*)ws;
   float* scales = (float*)(ws + align256(amax_partial_words(B, H) * sizeof(uint32_t)));
   return quantize_all(in_dtype, o.q_scale_mode, B, H, D, N, M, q_train, k, v, q_test, q8_train, k8, v8, nullptr,
-                      q8_test, amax, scales, s_q, s_k, s_v, s_q_test, (hipStream_t)stream);
+                      q8_test, partial, scales, s_q, s_k, s_v, s_q_test, (hipStream_t)stream);
 }
 
 size_t tfm_icl_attention_fp8_workspace_bytes(int B, int H, int D, int N, int M) {
@@ -170,7 +170,7 @@ int tfm_icl_attention_fp8_quantize(int in_dtype, const tfm_icl_options* opts, in
   if (workspace_bytes < L.total) return TFM_ERR_WORKSPACE_TOO_SMALL;
   uint8_t* ws = (uint8_t*)workspace;
   return quantize_all(in_dtype, o.q_scale_mode, B, H, D, N, M, q_train, k, v, q_test, ws + L.q8_train, ws + L.k8,
-                      nullptr, ws + L.v8t, ws + L.q8_test, (uint32_t*)(ws + L.amax), (float*)(ws + L.scales),
+                      nullptr, ws + L.v8t, ws + L.q8_test, (uint32_t*)(ws + L.partial), (float*)(ws + L.scales),
                       nullptr, nullptr, nullptr, nullptr, (hipStream_t)stream);
 }
 
@@ -234,7 +234,7 @@ int tfm_icl_attention_fp8_fit(int in_dtype, int out_dtype, const tfm_icl_options
   float* scales = (float*)(ws + L.scales);
   const int BH = B * H;
   TFM_TRY(quantize_all(in_dtype, TFM_QSCALE_SHARED, B, H, D, N, 0, q_train, k, v, nullptr, ws + L.q8_train,
-                       ws + L.k8, nullptr, ws + L.v8t, nullptr, (uint32_t*)(ws + L.amax), scales, nullptr, nullptr,
+                       ws + L.k8, nullptr, ws + L.v8t, nullptr, (uint32_t*)(ws + L.partial), scales, nullptr, nullptr,
                        nullptr, nullptr, s));
   return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTrain, B, H, D, N, 0, o.test_kv_heads, alpha,
                                     ws + L.q8_train, nullptr, ws + L.k8, ws + L.v8t, scales, scales + BH,
@@ -259,16 +259,16 @@ int tfm_icl_attention_fp8_predict(int in_dtype, int out_dtype, const tfm_icl_opt
   if (M == 0) return TFM_OK;
   uint8_t* ws = (uint8_t*)workspace;
   hipStream_t s = (hipStream_t)stream;
-  uint32_t* amax = (uint32_t*)(ws + L.amax);
+  uint32_t* partial = (uint32_t*)(ws + L.partial);
   float* scales = (float*)(ws + L.scales);
   const int bf = in_dtype == TFM_BF16;
   const int BH = B * H;
   if (o.q_scale_mode == TFM_QSCALE_PER_CALL)
-    TFM_HIP(launch_amax(bf, 3, 3, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, amax, s));
+    TFM_HIP(launch_amax(bf, 3, 3, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, partial, s));
   // Under the shared scale s_q_test comes from the fit's Q_train slice maxima, which the
   // workspace still holds; s_q, s_k and s_v stay as the fit stored them.
   TFM_HIP(launch_quantize(bf, o.q_scale_mode, B, H, D, N, M, nullptr, nullptr, nullptr, q_test, nullptr, nullptr,
-                          nullptr, nullptr, ws + L.q8_test, amax, scales, nullptr, nullptr, nullptr, nullptr, s));
+                          nullptr, nullptr, ws + L.q8_test, partial, scales, nullptr, nullptr, nullptr, nullptr, s));
   return hip_status(launch_attn_fp8(out_dtype == TFM_BF16, kCallTest, B, H, D, N, M, o.test_kv_heads, alpha,
                                     ws + L.q8_train, ws + L.q8_test, ws + L.k8, ws + L.v8t, scales, scales + BH,
                                     scales + 2 * BH, scales + 3 * BH, nullptr, o_test, s));

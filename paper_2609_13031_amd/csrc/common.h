@@ -42,7 +42,7 @@ inline size_t amax_partial_words(int B, int H) { return (size_t)4 * B * H * kAma
 // Byte offsets of the pieces of the FP8 workspace (all 256-byte aligned).  Everything
 // before q8_test depends on the train rows only (the state a fit call leaves behind).
 struct Fp8Workspace {
-  size_t amax;      // [4][B][H][kAmaxSlices] uint32: slice maxima of |x| (float bits) of Q_train, K, V, Q_test
+  size_t partial;   // [4][B][H][kAmaxSlices] uint32: slice maxima of |x| (float bits) of Q_train, K, V, Q_test
   size_t scales;    // 4*B*H float: s_q, s_k, s_v, s_q_test
   size_t q8_train;  // (B,H,N,D) codes
   size_t k8;        // (B,H,N,D) codes
