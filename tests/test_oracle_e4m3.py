@@ -42,6 +42,11 @@ def test_worked_values():
 def _tie_sensitive_patterns():
     # every fp32 bit pattern's upper 16 bits with lower halves that put the
     # discarded bits at 0, 1 ulp, just below / at / above half, and all ones.
+    # This is as strong as trying all 2^32 patterns: an e4m3 result keeps at
+    # most 3 mantissa bits, so the rounding bit of a fp32 input is mantissa bit
+    # 19 or higher (higher still for subnormal results), inside the upper 16
+    # bits; the lower 16 bits can only act as sticky bits, where all that counts
+    # is whether they are zero, and every upper half is tried with both.
     hi = np.arange(1 << 16, dtype=np.uint32) << 16
     lows = np.array([0, 1, 0x7FFF, 0x8000, 0x8001, 0xFFFF], dtype=np.uint32)
     u = (hi[:, None] | lows[None, :]).ravel()
