@@ -28,16 +28,28 @@ T1_MAX, T1_RELF, T1_OUTLIER, T1_OUTLIER_FRAC = 1e-2, 1e-4, 2e-3, 1e-3   # report
 # the first with a 2x margin, EPS_ACC the second per key tile.
 EPS_DOT = 2.0 ** -11
 EPS_ACC = 2.0 ** -22
-# T1' -- on general inputs the FP8 path stays within relF 3e-2 of O_qp, and
-# elementwise within T2' of O_q.  The dot-product error above usually gives
-# ~1e-3.  It gives more on heads whose logits are both huge and sharp:
-# outlier channels in Q and in K push sum |q_k k_k| to 2e5 on one head of a
-# random-shape case (B=3, H=7, N=337, bf16, seed 1004), where 2^-11 of it is
-# 0.8 log2 units of logit and the rows span hundreds; the kernel is at relF
-# 1.1e-2 there, an emulated truncation of the products to 15 bits of the largest
-# moves O_qp by 1.4e-2, and T2' holds on every row.  A dropped key tile or a
-# missing rescale gives 0.17 and more.
-T1P_RELF = 3e-2
+# T1' -- on general inputs the FP8 path stays within relF 2e-2 of O_qp (a
+# dropped key tile or a missing rescale gives 0.17 and more), on heads whose
+# logits the dot-product error above can move by at most T1P_MAX_LOGIT_ERR
+# log2 units: delta = c * EPS_DOT * max_ij sum_k |q_ik k_jk|, from the codes.
+# Typical heads of the workloads have delta ~0.1.  Over 160 seeded random
+# cases (B <= 4, H <= 9, N up to 6000, multipliers up to 8, outliers up to 50x)
+# the worst such head per case had median relF 1e-3, 90th percentile 4e-3 and
+# maximum 1.07e-2, from rows whose two leading keys are within delta.  Where
+# the outlier channels of Q and K coincide, sum |q_k k_k| reaches 1e5 and more
+# and delta 1 to 7 log2 units, on rows whose logits span hundreds or
+# thousands: two leading keys closer than delta may then swap which dominates,
+# such a row's output moves by up to a few RMS (relF 1e-2 to 4e-2 measured),
+# and only the elementwise T2', which bounds exactly that error, is a test;
+# it is then required on every checked row instead.  An emulation that
+# truncates the products to 15 bits of the largest moves O_qp by the same
+# amounts on such heads.
+# relF is a statistic of the rows checked: with few of them a single row whose
+# leading keys are within delta dominates it (relF 2e-2 from one of 12 test
+# rows in one case), so T1' also needs at least T1P_MIN_ROWS rows.
+T1P_RELF = 2e-2
+T1P_MAX_LOGIT_ERR = 0.25
+T1P_MIN_ROWS = 32
 
 
 def t1_metrics(got, ref):
@@ -55,6 +67,40 @@ def assert_t1(got, ref, allowance, what=""):
     tol = 1.01 * allowance + 1e-5 * rms + 1e-6 * np.abs(ref)
     assert np.all(err <= tol), (what, (err / tol).max(), t1_metrics(got, ref))
     return t1_metrics(got, ref)
+
+
+def _abs_dev_sums(v, o):
+    """out[r, c] = sum_j |v[j, c] - o[r, c]|, from each channel's sorted values and prefix sums."""
+    N = v.shape[0]
+    vs = np.sort(np.ascontiguousarray(v.T), axis=1)      # (D, N): each channel's values in order
+    cs = np.empty((vs.shape[0], N + 1))
+    cs[:, 0] = 0.0
+    np.cumsum(vs, axis=1, out=cs[:, 1:])
+    out = np.empty_like(o)
+    for ch in range(vs.shape[0]):
+        t = o[:, ch]
+        k = np.searchsorted(vs[ch], t)
+        out[:, ch] = t * k - cs[ch, k] + (cs[ch, N] - cs[ch, k]) - t * (N - k)
+    return out
+
+
+def _weighted_abs_dev(A, z, v, o):
+    """An upper bound of sum_j (A_rj + z_r) |v_jc - o_rc| (A >= 0, z >= 0), equal to it
+    up to 1e-9 relative.  The z part is summed over all keys with _abs_dev_sums; the A part
+    only over keys with A_rj >= 1e-16 max_j A_rj, and the rest of its mass is counted
+    at max_j |v_jc - o_rc|, so dropping them can only raise the result."""
+    num = z[:, None] * _abs_dev_sums(v, o)
+    vmax, vmin = v.max(axis=0), v.min(axis=0)
+    N = v.shape[0]
+    for r in range(A.shape[0]):
+        keep = np.nonzero(A[r] >= 1e-16 * A[r].max())[0]
+        if len(keep) > N // 4:   # most keys count: sum over all of them, in cache-sized pieces
+            for j0 in range(0, N, 8192):
+                num[r] += A[r, j0:j0 + 8192] @ np.abs(v[j0:j0 + 8192] - o[r])
+        else:
+            num[r] += A[r, keep] @ np.abs(v[keep] - o[r])
+            num[r] += (A[r].sum() - A[r, keep].sum()) * np.maximum(vmax - o[r], o[r] - vmin)
+    return num * (1 + 1e-9)
 
 
 def p_rounding_bound(q8, k8, v_hat, c, eps_dot=0.0, n_tiles=0):
@@ -75,11 +121,11 @@ def p_rounding_bound(q8, k8, v_hat, c, eps_dot=0.0, n_tiles=0):
     psum = p.sum(axis=1)
     o = (p @ v_hat) / psum[:, None]
     a = np.abs(q8) @ np.abs(k8).T
-    e = p * ((1 + 2.0 ** -4) * np.exp2(c * eps_dot * a) - 1) + 2.0 ** -10 * np.exp2(c * eps_dot * a.max(axis=1))[:, None]
-    num = np.empty_like(o)
-    for ch in range(v_hat.shape[1]):
-        num[:, ch] = np.einsum("rj,rj->r", e, np.abs(v_hat[None, :, ch] - o[:, ch][:, None]))
-    den = psum - e.sum(axis=1)
+    # e_rj = A_rj + z_r: the weight term and the subnormal term, the same for every key
+    A = p * ((1 + 2.0 ** -4) * np.exp2(c * eps_dot * a) - 1)
+    z = 2.0 ** -10 * np.exp2(c * eps_dot * a.max(axis=1))
+    num = _weighted_abs_dev(A, z, v_hat, o)
+    den = psum - (A.sum(axis=1) + z * k8.shape[0])
     bound = np.where(den[:, None] > 0, num / np.where(den > 0, den, 1.0)[:, None], np.inf)
     pv = (p @ np.abs(v_hat)) / psum[:, None]
     bound += (2 * eps_dot + n_tiles * EPS_ACC) * (pv + np.abs(o))
@@ -109,6 +155,32 @@ def assert_t1p(got, ref, what=""):
     m = t1_metrics(got, ref)
     assert m["relF"] <= T1P_RELF, (what, m)
     return m
+
+
+def logit_error_scale(qz, alpha, b, h, q8_rows, s_query=None, hk=None, eps_dot=EPS_DOT):
+    """delta = c * eps_dot * max over the rows and keys of sum_k |q_k k_k|: the most the FP8
+    dot-product error can move a base-2 logit of these rows (log2 units)."""
+    hk = h if hk is None else hk
+    s_query = qz["s_q"][b, h] if s_query is None else s_query
+    c = float(alpha) * float(s_query) * float(qz["s_k"][b, hk]) * OA.LOG2E
+    a = np.abs(decode(q8_rows)) @ np.abs(decode(qz["k8"][b, hk])).T
+    return c * eps_dot * float(a.max()) if a.size else 0.0
+
+
+def assert_t1p_or_t2(got, ref, qz, alpha, b, h, q8_rows, s_query=None, hk=None, what="", t2_max_rows=None):
+    """T1' against O_qp where the FP8 dot-product error moves logits by at most
+    T1P_MAX_LOGIT_ERR and at least T1P_MIN_ROWS rows are checked; otherwise T2'
+    against O_q on every row passed, or on t2_max_rows of them evenly spaced (the
+    bound costs rows * N * D, too much at 262144 keys for every sampled row).
+    Returns the metrics against O_qp and whether T1' applied."""
+    delta = logit_error_scale(qz, alpha, b, h, q8_rows, s_query, hk)
+    if delta <= T1P_MAX_LOGIT_ERR and len(q8_rows) >= T1P_MIN_ROWS:
+        return assert_t1p(got, ref, what), True
+    idx = np.arange(len(q8_rows))
+    if t2_max_rows is not None and len(idx) > t2_max_rows:
+        idx = np.unique(np.linspace(0, len(idx) - 1, t2_max_rows).astype(np.int64))
+    assert_t2(np.asarray(got)[idx], qz, alpha, b, h, np.asarray(q8_rows)[idx], s_query=s_query, hk=hk)
+    return t1_metrics(got, ref), False
 
 
 def narrow_range_inputs(B, N, M, H, D, seed):

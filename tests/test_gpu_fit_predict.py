@@ -11,7 +11,7 @@ from oracle import attention as OA
 from oracle import quantize as OQ
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import Workload, generate
-from parity import assert_t1p, assert_t2, gpu_inputs
+from parity import assert_t1p_or_t2, assert_t2, gpu_inputs
 
 pytestmark = pytest.mark.gpu
 BKV = 128
@@ -67,8 +67,10 @@ def test_per_call_predict_follows_the_oracle(table):
     r_tr, r_te = OA.icl_attention_fp8_kernel_model(qz, w.alpha, BKV, [], None)
     for b in range(w.B):
         for h in range(w.H):
-            assert_t1p(o_te[b, :, h], r_te[b, :, h], (b, h))
-            assert_t2(o_te[b, :40, h], qz, w.alpha, b, h, qz["q8_test"][b, h, :40], s_query=qz["s_q_test"][b, h])
+            _, t1 = assert_t1p_or_t2(o_te[b, :, h], r_te[b, :, h], qz, w.alpha, b, h, qz["q8_test"][b, h],
+                                     s_query=qz["s_q_test"][b, h], what=(b, h))
+            if t1:
+                assert_t2(o_te[b, :40, h], qz, w.alpha, b, h, qz["q8_test"][b, h, :40], s_query=qz["s_q_test"][b, h])
 
 
 def test_fit_predict_edge_cases(table):

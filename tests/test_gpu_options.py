@@ -10,7 +10,7 @@ from oracle import attention as OA
 from oracle import quantize as OQ
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import Workload, generate
-from parity import TIE_REL, assert_t1, assert_t1p, assert_t2, gpu_inputs, narrow_range_inputs, sample_rows
+from parity import TIE_REL, assert_t1, assert_t1p_or_t2, assert_t2, gpu_inputs, narrow_range_inputs, sample_rows
 
 pytestmark = pytest.mark.gpu
 BKV = 128
@@ -79,8 +79,10 @@ def test_fp8_attention_modes_and_grouped_test_heads(mode, G):
     for b in range(w.B):
         for h in range(w.H):
             hk = OA.grouped_kv_head(h, w.H, G or None)
-            assert_t1p(o_tr[b, rt, h], r_tr[b, :, h], ("train", mode, G, b, h))
-            assert_t1p(o_te[b, re, h], r_te[b, :, h], ("test", mode, G, b, h))
+            assert_t1p_or_t2(o_tr[b, rt, h], r_tr[b, :, h], qz, w.alpha, b, h, qz["q8_train"][b, h, rt],
+                             what=("train", mode, G, b, h))
+            assert_t1p_or_t2(o_te[b, re, h], r_te[b, :, h], qz, w.alpha, b, h, qz["q8_test"][b, h, re],
+                             s_query=qz["s_q_test"][b, h], hk=hk, what=("test", mode, G, b, h))
             assert_t2(o_tr[b, rt[:16], h], qz, w.alpha, b, h, qz["q8_train"][b, h, rt[:16]])
             assert_t2(o_te[b, re[:16], h], qz, w.alpha, b, h, qz["q8_test"][b, h, re[:16]],
                       s_query=qz["s_q_test"][b, h], hk=hk)
@@ -174,5 +176,7 @@ def test_many_heads_and_row_slices(mode):
     a_tr, a_te = a_tr.cpu().numpy(), a_te.cpu().numpy()
     for b in range(w.B):
         for j, h in enumerate(heads):
-            assert_t1p(a_tr[b, rt, h], r_tr[b, :, j], ("train", mode, b, h))
-            assert_t1p(a_te[b, re, h], r_te[b, :, j], ("test", mode, b, h))
+            assert_t1p_or_t2(a_tr[b, rt, h], r_tr[b, :, j], sub, w.alpha, b, j, sub["q8_train"][b, j, rt],
+                             what=("train", mode, b, h))
+            assert_t1p_or_t2(a_te[b, re, h], r_te[b, :, j], sub, w.alpha, b, j, sub["q8_test"][b, j, re],
+                             s_query=sub["s_q_test"][b, j], what=("test", mode, b, h))
