@@ -20,9 +20,8 @@ MAX_FINITE = 448.0
 NAN_CODES = (0x7F, 0xFF)
 
 
-def decode(codes):
-    """Value (float64) of each e4m3fn code; NaN for 0x7F / 0xFF."""
-    c = np.asarray(codes, dtype=np.uint8).astype(np.int64)
+def _decode_codes(c):
+    """The definition above, applied to int64 codes."""
     sign = np.where(c & 0x80, -1.0, 1.0)
     e = (c >> 3) & 0xF
     m = (c & 0x7).astype(np.float64)
@@ -31,18 +30,17 @@ def decode(codes):
     return sign * mag
 
 
-def encode_rne(y):
-    """e4m3fn code (uint8) of each finite y with |y| <= 448, nearest-even.
+# the value of every code, so that decoding an array is a lookup (same values)
+_VALUES = _decode_codes(np.arange(256, dtype=np.int64))
 
-    y may be float32 or float64; it is widened to float64 exactly.  For a
-    normal target the magnitude is written a = 2^e * q / 8 with q in [8, 16);
-    q is rounded half-to-even to an integer (a power-of-two scaling, so the
-    rounding is of y itself), and a carry to 16 moves to the next binade.
-    Below 2^-6 the spacing is the subnormal step 2^-9.
-    """
-    y = np.asarray(y, dtype=np.float64)
-    if not np.all(np.isfinite(y)) or np.any(np.abs(y) > MAX_FINITE):
-        raise ValueError("encode_rne needs finite inputs with |y| <= 448")
+
+def decode(codes):
+    """Value (float64) of each e4m3fn code; NaN for 0x7F / 0xFF."""
+    return _VALUES[np.asarray(codes, dtype=np.uint8)]
+
+
+def _encode_block(y):
+    """encode_rne on a float64 array (no checks)."""
     a = np.abs(y)
     code = np.zeros(a.shape, dtype=np.int64)
 
@@ -61,6 +59,29 @@ def encode_rne(y):
 
     code = code | np.where(np.signbit(y), 0x80, 0)
     return code.astype(np.uint8)
+
+
+def encode_rne(y):
+    """e4m3fn code (uint8) of each finite y with |y| <= 448, nearest-even.
+
+    y may be float32 or float64; it is widened to float64 exactly.  For a
+    normal target the magnitude is written a = 2^e * q / 8 with q in [8, 16);
+    q is rounded half-to-even to an integer (a power-of-two scaling, so the
+    rounding is of y itself), and a carry to 16 moves to the next binade.
+    Below 2^-6 the spacing is the subnormal step 2^-9.  Each element is coded
+    on its own; large arrays go through in pieces of 2^18 elements only to keep
+    the temporaries small.
+    """
+    y = np.asarray(y)
+    flat = y.reshape(-1)
+    out = np.empty(flat.shape, dtype=np.uint8)
+    piece = 1 << 18
+    for i in range(0, flat.size, piece):
+        yi = flat[i:i + piece].astype(np.float64)
+        if not np.all(np.abs(yi) <= MAX_FINITE):   # also false for NaN
+            raise ValueError("encode_rne needs finite inputs with |y| <= 448")
+        out[i:i + piece] = _encode_block(yi)
+    return out.reshape(y.shape)
 
 
 def round_to_e4m3(y):

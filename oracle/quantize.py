@@ -53,8 +53,11 @@ def quantize_with_scale(x, s):
     """Codes rn_fp8(clamp(fl32(x / s), -448, 448)): (B,S,H,D), (B,H) -> (B,H,S,D) uint8."""
     x = np.asarray(x, dtype=np.float32)
     s = np.asarray(s, dtype=np.float32)
-    y = np.divide(x, s[:, None, :, None], dtype=np.float32)
-    y = np.clip(y, -MAX_FINITE, MAX_FINITE)
+    # a value far outside the scale's range (test queries on the train-query scale)
+    # overflows fp32 to +-inf here; the clamp then saturates it to +-448
+    with np.errstate(over="ignore"):
+        y = np.divide(x, s[:, None, :, None], dtype=np.float32)
+    np.clip(y, np.float32(-MAX_FINITE), np.float32(MAX_FINITE), out=y)
     codes = encode_rne(y)
     return np.ascontiguousarray(codes.transpose(0, 2, 1, 3))
 
