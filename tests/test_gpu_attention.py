@@ -31,24 +31,33 @@ def fp8(g, w, out_dtype=torch.float32):
     return o[0].float().cpu().numpy(), o[1].float().cpu().numpy()
 
 
-def check_workload(w, rows_tr=None, rows_te=None, t2_rows=None):
+def run_workload(w):
+    """The fused FP8 call on the workload's inputs, and the oracle's codes and scales."""
     print("workload", w, flush=True)
     x = generate(w)
     g = gpu_inputs(x, torch.float32 if w.dtype == "f32" else torch.bfloat16)
     o_tr, o_te = fp8(g, w)
     del g
-    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    return o_tr, o_te, OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+
+
+def check_workload(w, rows_tr=None, rows_te=None, t2_rows=None, run=None, heads=None):
+    """T1'/T2' on the selected rows of heads [h0, h1) (default all) of every table."""
+    o_tr, o_te, qz = run_workload(w) if run is None else run
+    h0, h1 = (0, w.H) if heads is None else heads
+    qz = {k: v[:, h0:h1] for k, v in qz.items()}     # codes (B,H,S,D), scales (B,H)
+    o_tr, o_te = o_tr[:, :, h0:h1], o_te[:, :, h0:h1]
     r_tr, r_te = OA.icl_attention_fp8_kernel_model(qz, w.alpha, BKV, rows_tr, rows_te)
     rt = np.arange(w.N) if rows_tr is None else rows_tr
     re = np.arange(w.M) if rows_te is None else rows_te
     worst = 0.0
     for b in range(w.B):
-        for h in range(w.H):
+        for h in range(h1 - h0):
             for o, r, rows, q8 in ((o_tr, r_tr, rt, qz["q8_train"]), (o_te, r_te, re, qz.get("q8_test"))):
                 if len(rows) == 0:
                     continue
                 m, t1 = assert_t1p_or_t2(o[b, rows, h], r[b, :, h], qz, w.alpha, b, h, q8[b, h, rows],
-                                         what=(b, h, len(rows)), t2_max_rows=None if t2_rows is None else 2 * t2_rows)
+                                         what=(b, h0 + h, len(rows)), t2_max_rows=None if t2_rows is None else 2 * t2_rows)
                 if t1:   # otherwise T2' has just been checked on every row
                     worst = max(worst, m["relF"])
                     sub = rows if t2_rows is None else rows[:t2_rows]
@@ -92,12 +101,52 @@ def test_many_tables_sampled():
 
 def test_mid_full_size_sampled():
     w = WORKLOADS["mid"]
-    check_workload(w, sample_rows(w.N, 64, 5), sample_rows(w.M, 32, 6), t2_rows=8)
+    check_workload(w, sample_rows(w.N, 2048, 5), sample_rows(w.M, 512, 6), t2_rows=8)
 
 
-def test_large_full_size_sampled():
+@pytest.fixture(scope="module")
+def large_run():
+    return run_workload(WORKLOADS["large"])
+
+
+@pytest.mark.parametrize("heads", [(0, 4), (4, 8)])
+def test_large_full_size_sampled(large_run, heads):
     w = WORKLOADS["large"]
-    check_workload(w, sample_rows(w.N, 24, 7), sample_rows(w.M, 12, 8), t2_rows=4)
+    check_workload(w, sample_rows(w.N, 2048, 7), sample_rows(w.M, 512, 8), t2_rows=4, run=large_run, heads=heads)
+
+
+@pytest.mark.parametrize("name", ["mid", "large"])
+def test_full_size_every_row(name):
+    # Every output row at the full size, through properties that need no row of the
+    # oracle's attention.  (1) A row depends only on its own query (Eq. (1); the
+    # query scale comes from all of Q_train, which a permutation leaves alone), so
+    # permuting the query rows permutes the outputs bit for bit: a missed, repeated
+    # or misplaced query tile breaks this.  (2) A row is a mean of V-hat rows with
+    # weights >= 0, so each channel lies within V-hat's range over the keys, up to
+    # the FP8 MFMA error of the P V and row-sum products; NaN, garbage or a wrong
+    # output scale leaves that range.
+    w = WORKLOADS[name]
+    print("workload", w, flush=True)
+    x = generate(w)
+    g = gpu_inputs(x, torch.bfloat16)
+    a_tr, a_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    rng = np.random.default_rng(25)
+    p_tr = torch.from_numpy(rng.permutation(w.N)).cuda()
+    p_te = torch.from_numpy(rng.permutation(w.M)).cuda()
+    b_tr, b_te = tfm.tfm_icl_attention_fp8(g["q_train"][:, p_tr].contiguous(), g["k"], g["v"],
+                                           g["q_test"][:, p_te].contiguous(), alpha=w.alpha)
+    assert torch.equal(b_tr, a_tr[:, p_tr]) and torch.equal(b_te, a_te[:, p_te])
+    del b_tr, b_te, g
+    s_v = OQ.scale_from_amax(OQ.absmax_per_head(x["v"]))
+    v_hat = OA.dequantize(OQ.quantize_with_scale(x["v"], s_v), s_v)          # (B, N, H, D)
+    lo, hi = v_hat.min(axis=1), v_hat.max(axis=1)                            # (B, H, D)
+    del v_hat
+    slack = (2 * EPS_DOT + ((w.N + 63) // 64) * EPS_ACC) * 2 * np.maximum(np.abs(lo), np.abs(hi))
+    lo = torch.from_numpy(lo - slack).float().cuda()[:, None]
+    hi = torch.from_numpy(hi + slack).float().cuda()[:, None]
+    for o in (a_tr, a_te):
+        assert bool(torch.isfinite(o).all())
+        assert bool(((o >= lo) & (o <= hi)).all()), float(torch.maximum(lo - o, o - hi).max())
 
 
 @pytest.mark.parametrize("B,H,D,N,M,dtype", [
