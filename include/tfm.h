@@ -19,7 +19,13 @@
  * Conventions shared by every entry point
  * ---------------------------------------
  *  - B tables, H heads, D head_dim (64 or 128), N train rows (>= 1), M test
- *    rows (>= 0).  Activations are row-major (B, rows, H, D), the layout the
+ *    rows (>= 0), with B*H <= 65535 and N + M < 2^31 - 256.  Every launch
+ *    stays within 2^24 - 1 workgroups of 256 threads (2^32 work-items per grid
+ *    dimension): the attention grid has B*H*(ceil(N/128) + ceil(M/128)) query
+ *    tiles, and the quantize grid B*H*ceil(N/64) V tiles plus one workgroup
+ *    per 64 KiB of the other inputs, counted as fp32 whatever their dtype;
+ *    TFM_ERR_BAD_SHAPE otherwise.  One GPU's memory does not reach these
+ *    bounds.  Activations are row-major (B, rows, H, D), the layout the
  *    paper writes as X in R^{S x H x d}; quantized codes are row-major
  *    (B, H, rows, D) uint8; scales are (B, H) float32 dequantization scales.
  *  - All tensor pointers are device memory owned by the caller and borrowed
@@ -53,7 +59,7 @@ extern "C" {
 typedef enum {
   TFM_OK = 0,
   TFM_ERR_NULL_PTR = 1,             /* a required pointer is NULL */
-  TFM_ERR_BAD_SHAPE = 2,            /* B, H < 1, N < 1, M < 0, or a size overflows */
+  TFM_ERR_BAD_SHAPE = 2,            /* B, H < 1, N < 1, M < 0, or a size or grid overflows */
   TFM_ERR_BAD_DTYPE = 3,            /* dtype code not accepted by this entry point */
   TFM_ERR_UNSUPPORTED_HEAD_DIM = 4, /* D is not 64 or 128 */
   TFM_ERR_MISALIGNED = 5,           /* a pointer is not 16-byte aligned */
@@ -305,7 +311,9 @@ int tfm_icl_attention(int in_dtype, int out_dtype, const tfm_icl_options* opts, 
  *   workspace         >= tfm_noise_per_head_workspace_bytes(B, H, S, D) bytes
  *
  * D must be a multiple of 8 (TFM_ERR_UNSUPPORTED_HEAD_DIM otherwise);
- * H*D <= 16384, B*H <= 65535 and B*S*H*D <= 2^40 (TFM_ERR_BAD_SHAPE).
+ * H*D <= 16384, B*H <= 65535 and B*S*H*D below 2^37 (the elementwise pass
+ * launches one 256-thread workgroup per 8192 elements, at most 2^24 - 1 of
+ * them); TFM_ERR_BAD_SHAPE otherwise.
  * S == 0 is valid: nothing is read or written except rho, which is set to 0;
  * x, z, out and workspace may then be NULL.  Pointers 16-byte aligned.
  */

@@ -37,18 +37,19 @@ using namespace tfm;
 bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Shapes every entry point accepts.  Limits: B*H <= 65535 (a grid dimension),
-// N + M below INT_MAX - 256 (row indices are 32-bit), B*H*(ceil(N/128) +
-// ceil(M/128)) attention workgroups at most INT_MAX, and B*H*D*(N+M) elements
-// at most 2^48.
+// N + M below INT_MAX - 256 (row indices are 32-bit), and every grid within
+// kMaxGridBlocks workgroups: the attention grid of B*H*(ceil(N/128) +
+// ceil(M/128)) query tiles and the quantize grid, whose V part alone has
+// B*H*ceil(N/64) tiles (so the V relayout grid fits too).  The quantize grid is
+// counted for fp32 inputs, its largest, whatever the dtype of the call.
 int check_shape(int B, int H, int D, int N, int M) {
   if (B < 1 || H < 1 || N < 1 || M < 0) return TFM_ERR_BAD_SHAPE;
   if ((long long)B * H > 65535) return TFM_ERR_BAD_SHAPE;
   if ((long long)N + M > (long long)INT_MAX - 256) return TFM_ERR_BAD_SHAPE;
   if (D != 64 && D != 128) return TFM_ERR_UNSUPPORTED_HEAD_DIM;
-  if (((long long)N + 127) / 128 + ((long long)M + 127) / 128 > (long long)INT_MAX / ((long long)B * H))
+  if ((((long long)N + 127) / 128 + ((long long)M + 127) / 128) * B * H > kMaxGridBlocks)
     return TFM_ERR_BAD_SHAPE;  // attention grid: query tiles of the train rows, then of the test rows
-  const long double elems = (long double)B * H * D * ((long double)N + M);
-  if (elems > 281474976710656.0L) return TFM_ERR_BAD_SHAPE;
+  if (quantize_grid_blocks(4, B, H, D, N, M) > kMaxGridBlocks) return TFM_ERR_BAD_SHAPE;
   return TFM_OK;
 }
 
@@ -354,6 +355,7 @@ static int check_noise_shape(int B, int H, int S, int D) {
   if (D < 8 || D % 8 != 0) return TFM_ERR_UNSUPPORTED_HEAD_DIM;
   if ((long long)B * H > 65535 || (long long)H * D > 16384) return TFM_ERR_BAD_SHAPE;
   if ((long double)B * S * H * D > 1099511627776.0L) return TFM_ERR_BAD_SHAPE;  // 2^40 elements
+  if (noise_grid_blocks(B, H, S, D) > kMaxGridBlocks) return TFM_ERR_BAD_SHAPE;
   return TFM_OK;
 }
 

@@ -24,6 +24,9 @@ constexpr int kBlockKv = TFM_FP8_BLOCK_KV;  // keys per block (running-max granu
 constexpr float kLog2e = 1.4426950408889634f;
 // Which of the two ICL calls an attention launch runs (a mask).
 constexpr int kCallTrain = 1, kCallTest = 2;
+// Most workgroups of 256 threads in one grid dimension: a dispatch holds fewer than
+// 2^32 work-items per dimension.  The shape checks keep every launch within it.
+constexpr long long kMaxGridBlocks = 0xFFFFFFFFLL / 256;
 
 // The amax pass splits the rows of each (tensor, table) into at most kAmaxSlices
 // slices of at least kMinSliceRows rows and keeps one maximum per (slice, head).
@@ -72,6 +75,9 @@ hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, i
                            uint8_t* q8_train, uint8_t* k8, uint8_t* v8, uint8_t* v8t, uint8_t* q8_test,
                            const uint32_t* partial, float* scales, float* s_q, float* s_k, float* s_v,
                            float* s_q_test, hipStream_t s);
+// Workgroups of the largest launch_quantize grid for these shapes: all four tensors, V as
+// 64-key tiles, elements of esize bytes (fp32 inputs give the most).
+long long quantize_grid_blocks(int esize, int B, int H, int D, int N, int M);
 // Re-lay (B,H,N,D) V codes into the tile-transposed layout.
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8,
                                    uint8_t* v8t, hipStream_t s);
@@ -92,6 +98,8 @@ hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N
 // (chunks*B*H doubles), rho (B*H floats, also copied to rho_out when non-NULL),
 // then out = x + fl32(eps*rho)*z.  Requires S >= 1, D % 8 == 0, H*D <= 16384.
 int noise_rows_per_chunk(int H, int D);
+// Workgroups of the largest noise launch (the elementwise pass) for these shapes.
+long long noise_grid_blocks(int B, int H, int S, int D);
 hipError_t launch_noise(int x_bf16, int z_bf16, int B, int H, int S, int D, const void* x, const void* z, float eps,
                         void* out, double* partial, float* rho, float* rho_out, hipStream_t s);
 

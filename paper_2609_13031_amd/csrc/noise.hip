@@ -151,6 +151,14 @@ int noise_rows_per_chunk(int H, int D) {
   return r < 1 ? 1 : r;
 }
 
+long long noise_grid_blocks(int B, int H, int S, int D) {
+  const long long groups = (long long)B * S * H * D / kGroup;
+  const long long apply = (groups + kThreads * kPer - 1) / (kThreads * kPer);
+  const int rpc = noise_rows_per_chunk(H, D);
+  const long long chunks = ((long long)S + rpc - 1) / rpc;
+  return apply > chunks ? apply : chunks;
+}
+
 hipError_t launch_noise(int x_bf16, int z_bf16, int B, int H, int S, int D, const void* x, const void* z, float eps,
                         void* out, double* partial, float* rho, float* rho_out, hipStream_t s) {
   const int rpc = noise_rows_per_chunk(H, D);

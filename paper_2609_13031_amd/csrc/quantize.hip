@@ -376,6 +376,16 @@ int chunk_rows(int rows, int hn, int D, int esize) {
   return (int)r;
 }
 
+// Workgroups per table of one quantize segment: 64-key tiles of every head for V in
+// the tile layout, else row chunks of every head group.
+long long segment_blocks_per_table(int H, int D, int rows, int esize, bool v_tiles) {
+  if (rows <= 0) return 0;
+  if (v_tiles) return (long long)H * ((rows + 63) / 64);
+  const int hn = H < kHeadGroup ? H : kHeadGroup;
+  const int rpc = chunk_rows(rows, hn, D, esize);
+  return (long long)((rows + rpc - 1) / rpc) * head_groups(H);
+}
+
 __global__ void fill_zero_kernel(uint32_t* p, int n) {
   int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = 0u;
@@ -416,16 +426,17 @@ hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, i
   const int esize = in_bf16 ? 2 : 4;
   const int groups = head_groups(H);
   const int hn = H < kHeadGroup ? H : kHeadGroup;
-  long total = 0;
+  long long total = 0;
   a.nseg = 0;
   auto add = [&](const void* x, uint8_t* codes, float* s_out, int tensor, int v_tiles, int rows) {
     if (!x || rows <= 0) return;
     QSeg& g = a.seg[a.nseg++];
     g.x = x; g.codes = codes; g.s_out = s_out; g.tensor = tensor; g.v_tiles = v_tiles; g.rows = rows;
     g.rpc = chunk_rows(rows, hn, D, esize);
-    g.per_table = v_tiles ? H * ((rows + 63) / 64) : ((rows + g.rpc - 1) / g.rpc) * groups;
+    const long long per_table = segment_blocks_per_table(H, D, rows, esize, v_tiles);
+    g.per_table = (int)per_table;   // launched only when the whole grid fits (below)
     g.first = (int)total;
-    total += (long)B * g.per_table;
+    total += (long long)B * per_table;
   };
   // V, K, then the queries: the reverse of the order the amax pass reads them in, so the
   // second read of the most recently scanned tensors can still hit the memory-side cache
@@ -436,10 +447,15 @@ hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, i
   a.train_q_sets_test_slot = !(q_test && M > 0);
   if (a.nseg > 0 && a.seg[a.nseg - 1].tensor == 3) a.seg[a.nseg - 1].s_out = s_q_test;
   if (total == 0) return hipSuccess;
-  if (total > INT32_MAX) return hipErrorInvalidValue;
+  if (total > kMaxGridBlocks) return hipErrorInvalidValue;
   if (in_bf16) hipLaunchKernelGGL(quantize_kernel<uint16_t>, dim3((unsigned)total), dim3(kThreads), 0, s, a);
   else hipLaunchKernelGGL(quantize_kernel<float>, dim3((unsigned)total), dim3(kThreads), 0, s, a);
   return hipGetLastError();
+}
+
+long long quantize_grid_blocks(int esize, int B, int H, int D, int N, int M) {
+  return (long long)B * (segment_blocks_per_table(H, D, N, esize, true) + 2 * segment_blocks_per_table(H, D, N, esize, false) +
+                         segment_blocks_per_table(H, D, M, esize, false));
 }
 
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8, uint8_t* v8t, hipStream_t s) {

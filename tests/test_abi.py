@@ -88,6 +88,22 @@ def test_fp8_validation_errors(kw, status):
     assert fp8_call(**kw) == status
 
 
+def test_grid_limits_are_validated_before_any_launch():
+    # A launch holds fewer than 2^32 work-items per grid dimension: at 256 threads per
+    # workgroup, at most 16777215 workgroups.  Shapes whose attention or quantize grid
+    # would exceed that fail the shape check (the workspace here is always too small,
+    # so a shape that passes reports 6 and nothing is launched).
+    assert fp8_call(H=1, N=2 ** 29, M=0, q_test=None, o_test=None, nws=1000) == 6   # V: 2^23 tiles of 64 keys
+    assert fp8_call(H=1, N=2 ** 30, M=0, q_test=None, o_test=None, nws=1000) == 2   # V: 2^24 tiles
+    assert fp8_call(N=2 ** 20, M=2 ** 31 - 2 ** 20 - 1000, nws=1000) == 2      # 2 * 2^24 query tiles
+    assert fp8_call(N=2 ** 20, M=2 ** 20, nws=1000) == 6
+    assert tfm.tfm_icl_attention_fp8_workspace_bytes(1, 1, 64, 2 ** 30, 0) == 0
+    L = tfm.lib()
+    n = lambda S: L.tfm_noise_per_head(1, 1, 1, 1, S, 64, FAKE, FAKE, 0.1, FAKE, None, FAKE, 8, None)
+    assert n(2 ** 30) == 6            # 2^36 elements: 2^23 workgroups of 8192
+    assert n(2 ** 31 - 1) == 2        # just under 2^37 elements: 2^24 workgroups
+
+
 def test_validation_order_and_m_zero_allows_null_test_pointers():
     # M == 0: NULL test pointers are fine, so the next failing check (workspace) reports
     assert fp8_call(M=0, q_test=None, o_test=None, nws=10) == 6
