@@ -373,7 +373,9 @@ def main():
                                % (w.name, w.B, w.H, w.D, w.N, w.M, w.dtype),
                    "B": w.B, "H": w.H, "D": w.D, "N_train": w.N, "N_test": w.M, "in_dtype": w.dtype,
                    "out_dtype": "bf16", "parallelism": "single GPU"},
-        "stages_ms": {"quantize": round(quant_ms, 4), "attention": round(attn_ms, 4)},
+        "stages_ms": {"quantize": round(quant_ms, 4), "attention": round(attn_ms, 4),
+                      "quantize_median": round(float(np.median(q_ms)), 4),
+                      "attention_median": round(float(np.median(a_ms)), 4)},
         "speedup_vs_bf16": round(bf16["ms"] / ms_step, 3) if bf16 else None,
         "attention_only_speedup_vs_bf16": round(bf16["ms"] / attn_ms, 3) if bf16 else None,
         "bf16": bf16,

@@ -154,6 +154,22 @@ def test_kernel_model_lifts_row_max_to_256_and_weights_are_e4m3_values():
     assert np.allclose(p8, decode(encode_rne(np.round(p8, 9))), rtol=0, atol=1e-9)
 
 
+def test_running_max_lift_worked_example():
+    # One query, two blocks of two keys, c = 0.1 and one-hot V rows, so the output is the
+    # normalised weight vector.  In [128, 256) the e4m3 values are 16 apart, in [64, 128)
+    # 8 apart.  Block 1 (scores 0, -3): its running max is 0, the lifted weights are
+    # 2^8 = 256 and 2^7.7 = 207.9, which rounds to 208.  Block 2 (scores 15, 10): the max
+    # moves to 15, block 1's state is rescaled by 2^(0.1 (0 - 15)) = 2^-1.5, and the new
+    # weights are 256 and 2^7.5 = 181.0, which rounds to 176 (the midpoint to 192 is 184).
+    # A lift relative to the row's final max would give block 1 the weights 2^6.5 = 90.5
+    # -> 88 and 2^6.2 = 73.5 -> 72 instead of 256 r = 90.5 and 208 r = 73.5.
+    r = 2.0 ** -1.5
+    w = np.array([256 * r, 208 * r, 256.0, 176.0])
+    o = A.one_pass_fp8_attention(np.array([[1.0]]), np.array([[0.0], [-3.0], [15.0], [10.0]]), np.eye(4), 0.1,
+                                 1.0, 2)
+    assert np.allclose(o[0], w / w.sum(), rtol=1e-14, atol=0)
+
+
 def test_lift_keeps_subnormal_weights():
     # Base-2 logits 0 and -17.5: with the 2^8 lift the small weight is 2^-9.5, which
     # rounds to the smallest subnormal 2^-9 (a lift of 2^7 would round it to 0).

@@ -6,7 +6,7 @@ import os
 import numpy as np
 
 from oracle import quantize as Q
-from oracle.e4m3 import decode
+from oracle.e4m3 import decode, encode_rne
 
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden", "quantization_error.txt")
 
@@ -51,6 +51,27 @@ def test_fp32_division_is_correctly_rounded():
     x = rng.standard_normal(1_000_000).astype(np.float32) * np.float32(50)
     s = np.float32(0.0123456)
     assert np.array_equal(np.divide(x, s, dtype=np.float32), (x.astype(np.float64) / np.float64(s)).astype(np.float32))
+
+
+def test_quantizer_divides_where_the_reciprocal_would_move_a_tie():
+    # Eq. (2) divides by s.  Inputs x = fl32(t s) for which the IEEE quotient x / s is
+    # exactly an e4m3 rounding midpoint t, but x * fl32(1/s) is one fp32 ulp off it, so
+    # a reciprocal multiply would round to the other neighbour where the tie goes down.
+    rng = np.random.default_rng(31)
+    mids = np.array([(1 + (2 * m + 1) / 16) * 2.0 ** e for e in range(-3, 8) for m in range(8)
+                     if (1 + (2 * m + 1) / 16) * 2.0 ** e < 448])
+    found = []
+    for s in rng.uniform(1e-3, 10.0, 3000).astype(np.float32):
+        x = (mids * np.float64(s)).astype(np.float32)
+        exact = (x.astype(np.float64) / np.float64(s)).astype(np.float32)
+        recip = x * (np.float32(1.0) / s)
+        for i in np.nonzero((exact == mids) & (recip != exact))[0]:
+            found.append((x[i], s))
+    assert len(found) > 50
+    for x, s in found:
+        code = Q.quantize_with_scale(np.full((1, 1, 1, 1), x, np.float32), np.full((1, 1), s, np.float32))
+        want = encode_rne(np.float32(np.float64(x) / np.float64(s)))
+        assert code[0, 0, 0, 0] == want, (x, s)
 
 
 def test_power_of_two_equivariance():
