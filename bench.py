@@ -243,7 +243,7 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mid")
-    ap.add_argument("--cpu-rows", type=int, default=8192, help="query rows of the oracle sample")
+    ap.add_argument("--cpu-rows", type=int, default=12288, help="query rows of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--accuracy-rows", type=int, default=1024,
                     help="rows of the oracle sample also compared with fp64 attention (with the CPU baseline)")
