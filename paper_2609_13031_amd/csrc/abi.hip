@@ -38,8 +38,8 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 // Shapes every entry point accepts.  Limits: B*H <= 65535 (a grid dimension),
 // N + M below INT_MAX - 256 (row indices are 32-bit), and every grid within
-// kMaxGridBlocks workgroups: the attention grid of B*H*(ceil(N/128) +
-// ceil(M/128)) query tiles and the quantize grid, whose V part alone has
+// kMaxGridBlocks workgroups: the attention grid of at most B*H*(ceil(N/128) +
+// ceil(M/128)) query tiles (128 or 256 rows each) and the quantize grid, whose V part alone has
 // B*H*ceil(N/64) tiles (so the V relayout grid fits too).  The quantize grid is
 // counted for fp32 inputs, its largest, whatever the dtype of the call.
 int check_shape(int B, int H, int D, int N, int M) {

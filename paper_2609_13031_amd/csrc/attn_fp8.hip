@@ -1,12 +1,16 @@
 // Fused FP8 ICL attention on gfx950 (train-train and test-train in one launch).
 //
 // The kernel of Sec. 3 / Fig. 2 of the paper, laid out for CDNA4:
-//  * a workgroup of 4 wave64s owns 128 consecutive train rows or 128
-//    consecutive test rows of one (b, h) (both ICL calls share K_8 and V_8,
-//    so they are one launch; the grid lists the train tiles of each (b, h),
-//    then its test tiles, and a launch may run only one of the two calls);
-//    each wave owns 32 rows; test rows may attend to a shared K/V head
-//    (grouped-query test-train call);
+//  * a workgroup of W wave64s owns 32 W consecutive train rows or test rows
+//    of one (b, h) (both ICL calls share K_8 and V_8, so they are one
+//    launch; the grid lists the train tiles of each (b, h), then its test
+//    tiles, and a launch may run only one of the two calls); each wave owns
+//    32 rows; test rows may attend to a shared K/V head (grouped-query
+//    test-train call).  W = 4 at head dimension 64 (three workgroups per CU,
+//    3 waves per SIMD).  At 128, W = 8 (one workgroup per CU, 2 waves per
+//    SIMD: sharing each staged key block among twice the rows measured 7-14%
+//    faster) when that grid still gives every CU a workgroup, else W = 4 (two
+//    per CU).  W changes no output bit: every decision is per wave;
 //  * keys are processed in blocks of kBlockKv (128), staged through LDS with
 //    double buffering: the global loads of block k+1 are issued before the
 //    math of block k and written to the other buffer after it, one barrier
@@ -35,9 +39,8 @@
 namespace tfm {
 namespace {
 
-constexpr int kWaves = 4;
 constexpr int kRowsPerWave = 32;
-constexpr int kRowsPerBlock = kWaves * kRowsPerWave;
+constexpr int kComputeUnits = 256;   // MI355X; the wave-count choice below only affects speed
 constexpr int kPad = 16;  // padded-layout LDS row padding (bytes): conflict-free 16-byte lane reads
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
@@ -101,18 +104,18 @@ __device__ inline int lds_off(int r, int c) {
 // Copy key block kb straight from global memory into LDS (global_load_lds_dwordx4:
 // lane l of a wave instruction writes LDS bytes [base + 16 l, +16)): K as BKV rows
 // of D bytes, V^T as BKV/64 stacked tiles of D rows of 64 bytes.  The 1024-byte
-// pieces are shared out over the 4 waves.  Keys >= N read row N-1 and 64-key tiles
+// pieces are shared out over the W waves.  Keys >= N read row N-1 and 64-key tiles
 // past the end read the last tile: their scores are masked to -inf, so their
 // weights are exactly 0.
-template <int D, int BKV>
+template <int D, int BKV, int W>
 __device__ inline void stage_dma(const uint8_t* kbase, const uint8_t* vbase, int kb, int N, int ntiles64,
                                  uint8_t* k_lds, uint8_t* v_lds, int wave, int lane) {
   constexpr int NP = BKV / 64;
   constexpr int KPIECES = BKV * D / 1024, VPIECES = NP * D * 64 / 1024;
-  static_assert(KPIECES % kWaves == 0 && VPIECES % kWaves == 0, "pieces split evenly over the waves");
+  static_assert(KPIECES % W == 0 && VPIECES % W == 0, "pieces split evenly over the waves");
 #pragma unroll
-  for (int i = 0; i < KPIECES / kWaves; ++i) {
-    const int j = wave + kWaves * i;
+  for (int i = 0; i < KPIECES / W; ++i) {
+    const int j = wave + W * i;
     const int at = j * 1024 + lane * 16;
     const int r = at / D, pos = (at % D) >> 4;
     const int key = min(kb * BKV + r, N - 1);
@@ -120,8 +123,8 @@ __device__ inline void stage_dma(const uint8_t* kbase, const uint8_t* vbase, int
     __builtin_amdgcn_global_load_lds((global_void*)g, (lds_void*)(k_lds + j * 1024), 16, 0, 0);
   }
 #pragma unroll
-  for (int i = 0; i < VPIECES / kWaves; ++i) {
-    const int j = wave + kWaves * i;
+  for (int i = 0; i < VPIECES / W; ++i) {
+    const int j = wave + W * i;
     const int at = j * 1024 + lane * 16;
     const int r = at / 64, pos = (at % 64) >> 4;           // r = p * D + d
     const int t64 = min(kb * NP + r / D, ntiles64 - 1);
@@ -186,14 +189,15 @@ __device__ inline v8i load32_lds(const uint8_t* base, int r, int c0) {
   return v8i{(int)x.x, (int)x.y, (int)x.z, (int)x.w, (int)y.x, (int)y.y, (int)y.z, (int)y.w};
 }
 
-template <int D, int BKV, bool OUT_BF16>
-__global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
+template <int D, int BKV, bool OUT_BF16, int W>
+__global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
   constexpr int KD = D / 64;            // 64-wide head_dim chunks (k of one MFMA)
   constexpr int NS = BKV / 32;          // 32-key score tiles per key block
   constexpr int NP = BKV / 64;          // 64-key PV chunks per key block
   // D = 128: K/V copied into LDS by DMA, swizzled rows; D = 64: staged through
   // registers into padded rows (each measured the faster at its head dimension)
   constexpr bool kDma = D == 128;
+  static_assert(kDma || W == 4, "register staging spreads a key block over exactly 256 threads");
   constexpr int KBYTES = BKV * (kDma ? D : D + kPad), VBYTES = NP * D * (kDma ? 64 : 64 + kPad);
   constexpr int PIECES = BKV * D / 16 / 256;
   // two K/V stages: the next key block is written while the current one is read
@@ -208,7 +212,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
   // a workgroup serves either train rows (train-train call) or test rows (test-train call)
   const bool test = tile >= a.tiles_train;
   const int rows = test ? M : N;
-  const int row = (test ? tile - a.tiles_train : tile) * kRowsPerBlock + wave * kRowsPerWave + ql;
+  const int row = (test ? tile - a.tiles_train : tile) * (W * kRowsPerWave) + wave * kRowsPerWave + ql;
   const int bhkv = test ? b * a.H + h / a.test_group : bh;   // the (b, K/V head) the rows attend to
 
   // Q_8 fragment: lane holds head_dim bytes [64s + 32*half, +32) of its row
@@ -245,7 +249,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
 
   u32x4 kr[kDma ? 1 : PIECES], vr[kDma ? 1 : PIECES];
   if constexpr (kDma) {
-    stage_dma<D, BKV>(kbase, vbase, 0, N, ntiles64, lds, lds + KBYTES, wave, lane);
+    stage_dma<D, BKV, W>(kbase, vbase, 0, N, ntiles64, lds, lds + KBYTES, wave, lane);
     wait_dma();
   } else {
     stage_load<D, BKV>(kbase, vbase, 0, N, ntiles64, kr, vr);
@@ -260,7 +264,7 @@ __global__ __launch_bounds__(256, 2) void attn_fp8_kernel(Fp8Args a) {
     if (more) {
       if constexpr (kDma) {
         uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
-        stage_dma<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
+        stage_dma<D, BKV, W>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
       } else if ((kb + 2) * BKV <= N) {
         stage_load<D, BKV, true>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
       } else {
@@ -382,20 +386,29 @@ hipError_t launch_attn_fp8(int out_bf16, int calls, int B, int H, int D, int N, 
                            const float* s_q_test, void* o_train, void* o_test, hipStream_t s) {
   Fp8Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
-  a.tiles_train = (calls & kCallTrain) ? (N + kRowsPerBlock - 1) / kRowsPerBlock : 0;
-  a.tiles = a.tiles_train + ((calls & kCallTest) ? (M + kRowsPerBlock - 1) / kRowsPerBlock : 0);
+  auto tiles_of = [&](int rows_per_block) {
+    return (long long)((calls & kCallTrain) ? (N + rows_per_block - 1) / rows_per_block : 0) +
+           ((calls & kCallTest) ? (M + rows_per_block - 1) / rows_per_block : 0);
+  };
+  const bool wide = D == 128 && tiles_of(8 * kRowsPerWave) * B * H >= kComputeUnits;
+  const int rpb = (wide ? 8 : 4) * kRowsPerWave;
+  a.tiles_train = (calls & kCallTrain) ? (N + rpb - 1) / rpb : 0;
+  a.tiles = a.tiles_train + ((calls & kCallTest) ? (M + rpb - 1) / rpb : 0);
   if (a.tiles == 0) return hipSuccess;
   a.test_group = H / test_kv_heads;
   a.alpha = alpha;
   a.q8_train = q8_train; a.q8_test = q8_test; a.k8 = k8; a.v8t = v8t;
   a.s_q = s_q; a.s_k = s_k; a.s_v = s_v; a.s_q_test = s_q_test; a.o_train = o_train; a.o_test = o_test;
-  dim3 grid((unsigned)((long)a.tiles * B * H)), block(256);
+  dim3 grid((unsigned)((long)a.tiles * B * H)), block(rpb * 2);   // 64 threads per 32-row wave
   if (D == 64) {
-    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<64, kBlockKv, false, 4>), grid, block, 0, s, a);
+  } else if (wide) {
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, true, 8>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, false, 8>), grid, block, 0, s, a);
   } else {
-    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_fp8_kernel<128, kBlockKv, false, 4>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

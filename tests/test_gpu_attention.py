@@ -149,6 +149,13 @@ def test_full_size_every_row(name):
         assert bool(((o >= lo) & (o <= hi)).all()), float(torch.maximum(lo - o, o - hi).max())
 
 
+def test_d128_wide_workgroups_ragged_rows():
+    # B*H*ceil(rows/256) = 280 workgroups: the 8-wave kernel at head dimension 128, with a
+    # ragged last key block and partial last query tiles of both calls
+    w = Workload("wide", B=1, H=8, D=128, N=8300, M=300, dtype="bf16", seed=64)
+    check_workload(w, sample_rows(w.N, 256, 11), sample_rows(w.M, 64, 12), t2_rows=16)
+
+
 @pytest.mark.parametrize("B,H,D,N,M,dtype", [
     (1, 1, 64, 1, 1, "f32"), (1, 2, 64, 63, 0, "bf16"), (2, 1, 64, 64, 5, "f32"), (1, 3, 64, 65, 130, "bf16"),
     (1, 1, 128, 1, 0, "bf16"), (1, 2, 128, 129, 17, "f32"), (3, 2, 128, 200, 255, "bf16"), (1, 1, 64, 1000, 1, "bf16"),

@@ -36,6 +36,19 @@ def test_fit_then_predict_equals_the_fused_call(table, mode, G):
     assert torch.equal(o_te, f_te)
 
 
+def test_workgroup_width_at_d128_changes_no_bit():
+    # At head dimension 128 the fused call here runs workgroups of 8 waves (its grid still
+    # gives every compute unit one), while a 40-row predict batch runs workgroups of 4: the
+    # rows they share must agree bit for bit.
+    w = Workload("wide", B=1, H=8, D=128, N=8300, M=300, dtype="bf16", seed=63)
+    g = gpu_inputs(generate(w), torch.bfloat16)
+    f_tr, f_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    o_tr, ws = tfm.tfm_icl_attention_fp8_fit(g["q_train"], g["k"], g["v"], alpha=w.alpha, m_max=w.M)
+    part = tfm.tfm_icl_attention_fp8_predict(ws, g["q_test"][:, 17:57].contiguous(), w.N, alpha=w.alpha)
+    assert torch.equal(o_tr, f_tr)
+    assert torch.equal(part, f_te[:, 17:57])
+
+
 def test_predict_batches_are_independent_under_the_shared_scale(table):
     w, x, g = table
     _, ws = tfm.tfm_icl_attention_fp8_fit(g["q_train"], g["k"], g["v"], alpha=w.alpha, m_max=w.M)
