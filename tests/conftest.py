@@ -10,7 +10,6 @@ if ROOT not in sys.path:
 
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) and the built HIP library")
-    config.addinivalue_line("markers", "slow: long CPU test, excluded from the default CPU run")
     # A planted oracle mistake (tests/oracle_mutations.py), applied before any test
     # module imports the oracle; only the mutation check sets this, in a subprocess.
     mutation = os.environ.get("ORACLE_MUTATION")
