@@ -34,7 +34,7 @@ def draw_cases(n, seed):
     return cases
 
 
-@pytest.mark.parametrize("case", draw_cases(24, 80), ids=lambda c: "B%(B)dH%(H)dD%(D)dN%(N)dM%(M)d-%(dtype)s-%(mode)s-G%(G)d" % c)
+@pytest.mark.parametrize("case", draw_cases(40, 80), ids=lambda c: "B%(B)dH%(H)dD%(D)dN%(N)dM%(M)d-%(dtype)s-%(mode)s-G%(G)d" % c)
 def test_random_case(case):
     c = case
     w = Workload("random", B=c["B"], H=c["H"], D=c["D"], N=c["N"], M=c["M"], dtype=c["dtype"], seed=c["seed"])
@@ -66,3 +66,39 @@ def test_random_case(case):
                                  s_query=ref["s_q_test"][b, h], hk=hk, what=(c, "test", b, h))
                 assert_t2(o_te[b, :2, h], ref, w.alpha, b, h, ref["q8_test"][b, h, :2], s_query=ref["s_q_test"][b, h],
                           hk=hk)
+
+
+def draw_wide_cases(n, seed):
+    """Head dimension 128 with grids of at least 256 workgroups of 256 rows (the 8-wave kernel)."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    while len(cases) < n:
+        c = dict(B=int(rng.integers(2, 5)), H=int(rng.choice([8, 12, 16])), D=128, N=int(rng.integers(1500, 3200)),
+                 M=int(rng.integers(0, 700)), dtype=str(rng.choice(["f32", "bf16"])), mode=str(rng.choice(MODES)),
+                 seed=2000 + len(cases))
+        if c["B"] * c["H"] * (-(-c["N"] // 256) + -(-c["M"] // 256)) >= 256:
+            cases.append(c)
+    return cases
+
+
+@pytest.mark.parametrize("case", draw_wide_cases(8, 81), ids=lambda c: "B%(B)dH%(H)dN%(N)dM%(M)d-%(dtype)s-%(mode)s" % c)
+def test_random_wide_d128_case(case):
+    c = case
+    w = Workload("random", B=c["B"], H=c["H"], D=c["D"], N=c["N"], M=c["M"], dtype=c["dtype"], seed=c["seed"])
+    x = generate(w)
+    g = gpu_inputs(x, torch.float32 if c["dtype"] == "f32" else torch.bfloat16)
+    q_test = g["q_test"] if c["M"] else None
+    o_tr, o_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], q_test, alpha=w.alpha, q_scale_mode=c["mode"])
+    o_tr, o_te = o_tr.cpu().numpy(), o_te.cpu().numpy()
+    ref = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"] if c["M"] else None,
+                                   q_scale_mode=c["mode"])
+    rt = np.unique(np.concatenate([np.arange(0, w.N, 37), [w.N - 1]]))
+    re = np.unique(np.concatenate([np.arange(0, w.M, 23), [w.M - 1]])) if c["M"] else np.zeros(0, np.int64)
+    r_tr, r_te = OA.icl_attention_fp8_kernel_model(ref, w.alpha, tfm.tfm_icl_attention_fp8_block_kv(w.D), rt, re)
+    for b in range(w.B):
+        for h in range(w.H):
+            assert_t1p_or_t2(o_tr[b, rt, h], r_tr[b, :, h], ref, w.alpha, b, h, ref["q8_train"][b, h, rt],
+                             what=(c, "train", b, h), t2_max_rows=8)
+            if c["M"]:
+                assert_t1p_or_t2(o_te[b, re, h], r_te[b, :, h], ref, w.alpha, b, h, ref["q8_test"][b, h, re],
+                                 s_query=ref["s_q_test"][b, h], what=(c, "test", b, h), t2_max_rows=8)
