@@ -20,10 +20,12 @@
  * ---------------------------------------
  *  - B tables, H heads, D head_dim (64 or 128), N train rows (>= 1), M test
  *    rows (>= 0), with B*H <= 65535 and N + M < 2^31 - 256.  Every launch
- *    stays within 2^24 - 1 workgroups of 256 threads (2^32 work-items per grid
- *    dimension): the attention grid has at most B*H*(ceil(N/128) + ceil(M/128))
- *    query tiles, and the quantize grid B*H*ceil(N/64) V tiles plus one workgroup
- *    per 64 KiB of the other inputs, counted as fp32 whatever their dtype;
+ *    stays below 2^32 work-items per grid dimension, so that counted in
+ *    workgroups of 256 threads, at most 2^24 - 1 of them: the attention grid
+ *    has B*H*(ceil(N/128) + ceil(M/128)) query tiles of 128 rows (at head
+ *    dimension 128, tiles of 256 rows are used only where they fit as well),
+ *    and the quantize grid B*H*ceil(N/64) V tiles plus one workgroup per
+ *    64 KiB of the other inputs, counted as fp32 whatever their dtype;
  *    TFM_ERR_BAD_SHAPE otherwise.  One GPU's memory does not reach these
  *    bounds.  Activations are row-major (B, rows, H, D), the layout the
  *    paper writes as X in R^{S x H x d}; quantized codes are row-major

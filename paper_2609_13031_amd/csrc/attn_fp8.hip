@@ -390,7 +390,9 @@ hipError_t launch_attn_fp8(int out_bf16, int calls, int B, int H, int D, int N, 
     return (long long)((calls & kCallTrain) ? (N + rows_per_block - 1) / rows_per_block : 0) +
            ((calls & kCallTest) ? (M + rows_per_block - 1) / rows_per_block : 0);
   };
-  const bool wide = D == 128 && tiles_of(8 * kRowsPerWave) * B * H >= kComputeUnits;
+  // (the shape check bounds the 4-wave grid; the 8-wave one, of 512-thread blocks, is used only where it fits too)
+  const long long wide_blocks = tiles_of(8 * kRowsPerWave) * B * H;
+  const bool wide = D == 128 && wide_blocks >= kComputeUnits && wide_blocks <= kMaxGridBlocks / 2;
   const int rpb = (wide ? 8 : 4) * kRowsPerWave;
   a.tiles_train = (calls & kCallTrain) ? (N + rpb - 1) / rpb : 0;
   a.tiles = a.tiles_train + ((calls & kCallTest) ? (M + rpb - 1) / rpb : 0);
