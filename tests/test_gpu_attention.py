@@ -156,6 +156,40 @@ def test_d128_wide_workgroups_ragged_rows():
     check_workload(w, sample_rows(w.N, 256, 11), sample_rows(w.M, 64, 12), t2_rows=16)
 
 
+def test_tensors_beyond_4_gib():
+    # B*H = 65408 heads of D = 128 and 640 train rows: every train-row tensor holds 5.4 G
+    # elements (10.7 GB in bf16, 5.4 GB of codes), so element and byte offsets pass 2^32.
+    # Inputs are drawn on the GPU; the heads at the start, the middle and the very end are
+    # checked against the oracle (codes and scales bit for bit, outputs within T1'/T2').
+    B, H, D, N, M = 511, 128, 128, 640, 64
+    gen = torch.Generator(device="cuda").manual_seed(65)
+    def draw(rows):
+        x = torch.randn((B, rows, H, D), generator=gen, device="cuda", dtype=torch.bfloat16)
+        x *= (torch.rand((B, 1, H, 1), generator=gen, device="cuda") * 3.5 + 0.5).to(torch.bfloat16)
+        return x
+    g = {"q_train": draw(N), "k": draw(N), "v": draw(N), "q_test": draw(M)}
+    alpha = np.float32(1.0 / np.sqrt(D))
+    qz = tfm.tfm_quantize_qkv_per_head(g["q_train"], g["k"], g["v"], g["q_test"])
+    assert qz["k8"].numel() > 2 ** 32 and qz["k8"].dtype == torch.uint8
+    o_tr, o_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=float(alpha))
+    assert o_tr.numel() > 2 ** 32
+    torch.cuda.synchronize()
+    for b, h in ((0, 0), (255, 77), (510, 126), (510, 127)):
+        x = {k: t[b:b + 1, :, h:h + 1].float().cpu().numpy() for k, t in g.items()}
+        ref = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+        for key in ("q8_train", "k8", "v8", "q8_test"):
+            assert np.array_equal(qz[key][b, h].cpu().numpy(), ref[key][0, 0]), (b, h, key)
+        for key in ("s_q", "s_k", "s_v", "s_q_test"):
+            assert qz[key][b, h].item() == ref[key][0, 0], (b, h, key)
+        r_tr, r_te = OA.icl_attention_fp8_kernel_model(ref, alpha, BKV)
+        assert_t1p_or_t2(o_tr[b, :, h].cpu().numpy(), r_tr[0, :, 0], ref, alpha, 0, 0, ref["q8_train"][0, 0],
+                         what=(b, h, "train"))
+        assert_t1p_or_t2(o_te[b, :, h].cpu().numpy(), r_te[0, :, 0], ref, alpha, 0, 0, ref["q8_test"][0, 0],
+                         s_query=ref["s_q_test"][0, 0], what=(b, h, "test"))
+    del g, qz, o_tr, o_te
+    torch.cuda.empty_cache()
+
+
 @pytest.mark.parametrize("B,H,D,N,M,dtype", [
     (1, 1, 64, 1, 1, "f32"), (1, 2, 64, 63, 0, "bf16"), (2, 1, 64, 64, 5, "f32"), (1, 3, 64, 65, 130, "bf16"),
     (1, 1, 128, 1, 0, "bf16"), (1, 2, 128, 129, 17, "f32"), (3, 2, 128, 200, 255, "bf16"), (1, 1, 64, 1000, 1, "bf16"),
