@@ -186,7 +186,17 @@ def test_tensors_beyond_4_gib():
                          what=(b, h, "train"))
         assert_t1p_or_t2(o_te[b, :, h].cpu().numpy(), r_te[0, :, 0], ref, alpha, 0, 0, ref["q8_test"][0, 0],
                          s_query=ref["s_q_test"][0, 0], what=(b, h, "test"))
-    del g, qz, o_tr, o_te
+    del qz, o_tr, o_te
+    # the 16-bit kernel on the same tensors, against Eq. (1) in fp64
+    b_tr, b_te = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=float(alpha))
+    torch.cuda.synchronize()
+    for b, h in ((0, 0), (510, 127)):
+        k, v = (g[n][b, :, h].double().cpu().numpy() for n in ("k", "v"))
+        for o, q in ((b_tr, g["q_train"]), (b_te, g["q_test"])):
+            ref, bnd = bf16_bound(q[b, :, h].double().cpu().numpy(), k, v, float(alpha))
+            err = np.abs(o[b, :, h].double().cpu().numpy() - ref)
+            assert np.all(err <= 1.25 * bnd + 1e-5 * np.sqrt(np.mean(ref ** 2))), (b, h)
+    del g, b_tr, b_te
     torch.cuda.empty_cache()
 
 
