@@ -98,3 +98,31 @@ def test_noise_full_size_keys_sampled_rows():
     n = gx.double().pow(2).sum(dim=(1, 3)).sqrt()
     rel = (d / n).cpu().numpy()
     assert np.all(np.abs(rel / 0.0265 - 1) < 0.1), rel
+
+
+def test_noise_beyond_4_gib():
+    # 8.6 G elements per tensor (B=2, S=2^21, H=16, D=128, bf16, drawn on the GPU): element and
+    # byte offsets pass 2^32.  rho of two heads (the first and the last) against the oracle over
+    # the whole head, and their outputs on sampled rows.
+    B, S, H, D = 2, 1 << 21, 16, 128
+    gen = torch.Generator(device="cuda").manual_seed(66)
+    gx = torch.randn((B, S, H, D), generator=gen, device="cuda", dtype=torch.bfloat16)
+    gx *= (10.0 ** (torch.rand((B, 1, H, 1), generator=gen, device="cuda") * 4 - 2)).to(torch.bfloat16)
+    gz = torch.randn((B, S, H, D), generator=gen, device="cuda", dtype=torch.bfloat16)
+    assert gx.numel() > 2 ** 32
+    eps = 0.05
+    out, rho = tfm.tfm_noise_per_head(gx, gz, eps)
+    torch.cuda.synchronize()
+    rows = sample_rows(S, 64, 67)
+    ri = torch.from_numpy(rows).cuda()
+    e = np.float64(np.float32(eps))
+    for b, h in ((0, 0), (1, 15)):
+        ref_rho = NZ.rms_per_head(gx[b, :, h].double().cpu().numpy()[None, :, None, :])[0, 0]
+        assert abs(rho[b, h].item() - ref_rho) <= (U + 1e-9) * ref_rho, (b, h)
+        x64, z64 = gx[b, ri, h].double().cpu().numpy(), gz[b, ri, h].double().cpu().numpy()
+        ref = x64 + e * ref_rho * z64
+        delta = 2.03 * U * e * ref_rho * np.abs(z64) + 1.0001 * U * np.abs(ref) + 1e-44
+        delta = delta + 2.0 ** -8 * (np.abs(ref) + delta)
+        assert np.all(np.abs(out[b, ri, h].double().cpu().numpy() - ref) <= delta), (b, h)
+    del gx, gz, out
+    torch.cuda.empty_cache()
