@@ -186,7 +186,11 @@ def test_tensors_beyond_4_gib():
                          what=(b, h, "train"))
         assert_t1p_or_t2(o_te[b, :, h].cpu().numpy(), r_te[0, :, 0], ref, alpha, 0, 0, ref["q8_test"][0, 0],
                          s_query=ref["s_q_test"][0, 0], what=(b, h, "test"))
-    del qz, o_tr, o_te
+    # the prequantized entry point (public code layout, V re-laid into tiles) gives every row bit for bit
+    p_tr, p_te = tfm.tfm_icl_attention_fp8_prequantized(qz["q8_train"], qz["k8"], qz["v8"], qz["q8_test"], qz["s_q"],
+                                                        qz["s_k"], qz["s_v"], alpha=float(alpha))
+    assert torch.equal(p_tr, o_tr) and torch.equal(p_te, o_te)
+    del qz, o_tr, o_te, p_tr, p_te
     # the 16-bit kernel on the same tensors, against Eq. (1) in fp64
     b_tr, b_te = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=float(alpha))
     torch.cuda.synchronize()
