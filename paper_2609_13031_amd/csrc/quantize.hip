@@ -367,10 +367,19 @@ __global__ __launch_bounds__(kThreads) void relayout_v_tiles_kernel(int D, int N
     reinterpret_cast<u32x4*>(dst)[i] = reinterpret_cast<const u32x4*>(tile_codes)[i];
 }
 
-// Rows per quantize block: about 64 KiB of input (measured best among 64 KiB .. 512 KiB).
-int chunk_rows(int rows, int hn, int D, int esize) {
-  long per_row = (long)hn * D * esize;
-  long r = (65536 + per_row - 1) / per_row;
+// Input bytes per row-layout quantize block: 64 KiB (measured best among 64 KiB .. 512 KiB
+// on large inputs), down to 8 KiB for a small launch, so that it still has about four
+// blocks per CU and no block's chain of dependent loads sets the launch time.  The
+// blocking changes no code.
+long long chunk_target_bytes(long long launch_input_bytes) {
+  const long long t = launch_input_bytes / (4 * 256);
+  return t < 8192 ? 8192 : t > 65536 ? 65536 : t;
+}
+
+// Rows per row-layout quantize block at `target` input bytes per block.
+int chunk_rows(int rows, int hn, int D, int esize, long long target) {
+  long long per_row = (long long)hn * D * esize;
+  long long r = (target + per_row - 1) / per_row;
   if (r < 1) r = 1;
   if (r > rows) r = rows > 0 ? rows : 1;
   return (int)r;
@@ -378,11 +387,11 @@ int chunk_rows(int rows, int hn, int D, int esize) {
 
 // Workgroups per table of one quantize segment: 64-key tiles of every head for V in
 // the tile layout, else row chunks of every head group.
-long long segment_blocks_per_table(int H, int D, int rows, int esize, bool v_tiles) {
+long long segment_blocks_per_table(int H, int D, int rows, int esize, bool v_tiles, long long target) {
   if (rows <= 0) return 0;
   if (v_tiles) return (long long)H * ((rows + 63) / 64);
   const int hn = H < kHeadGroup ? H : kHeadGroup;
-  const int rpc = chunk_rows(rows, hn, D, esize);
+  const int rpc = chunk_rows(rows, hn, D, esize, target);
   return (long long)((rows + rpc - 1) / rpc) * head_groups(H);
 }
 
@@ -427,13 +436,16 @@ hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, i
   const int groups = head_groups(H);
   const int hn = H < kHeadGroup ? H : kHeadGroup;
   long long total = 0;
+  const long long launch_rows = (long long)(v ? N : 0) + (k ? N : 0) + (q_train ? N : 0) + (q_test ? M : 0);
+  const long long launch_bytes = (long long)B * H * D * esize * launch_rows;
+  const long long target = chunk_target_bytes(launch_bytes);
   a.nseg = 0;
   auto add = [&](const void* x, uint8_t* codes, float* s_out, int tensor, int v_tiles, int rows) {
     if (!x || rows <= 0) return;
     QSeg& g = a.seg[a.nseg++];
     g.x = x; g.codes = codes; g.s_out = s_out; g.tensor = tensor; g.v_tiles = v_tiles; g.rows = rows;
-    g.rpc = chunk_rows(rows, hn, D, esize);
-    const long long per_table = segment_blocks_per_table(H, D, rows, esize, v_tiles);
+    g.rpc = chunk_rows(rows, hn, D, esize, target);
+    const long long per_table = segment_blocks_per_table(H, D, rows, esize, v_tiles, target);
     g.per_table = (int)per_table;   // launched only when the whole grid fits (below)
     g.first = (int)total;
     total += (long long)B * per_table;
@@ -454,8 +466,12 @@ hipError_t launch_quantize(int in_bf16, int q_scale_mode, int B, int H, int D, i
 }
 
 long long quantize_grid_blocks(int esize, int B, int H, int D, int N, int M) {
-  return (long long)B * (segment_blocks_per_table(H, D, N, esize, true) + 2 * segment_blocks_per_table(H, D, N, esize, false) +
-                         segment_blocks_per_table(H, D, M, esize, false));
+  // the launch over all four tensors; a launch over fewer has less than 64 MiB of input
+  // where its chunks shrink, and then far fewer blocks than the limit
+  const long long target = chunk_target_bytes((long long)B * H * D * esize * (3LL * N + M));
+  return (long long)B * (segment_blocks_per_table(H, D, N, esize, true, target) +
+                         2 * segment_blocks_per_table(H, D, N, esize, false, target) +
+                         segment_blocks_per_table(H, D, M, esize, false, target));
 }
 
 hipError_t launch_relayout_v_tiles(int B, int H, int D, int N, const uint8_t* v8, uint8_t* v8t, hipStream_t s) {
