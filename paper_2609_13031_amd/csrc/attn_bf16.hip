@@ -3,8 +3,10 @@
 // The same two ICL calls as the FP8 kernel (N train + M test query rows of
 // each (b, h) against the same N train keys/values, Eq. (1) of the paper)
 // with the same structure, without quantization:
-//  * a workgroup of 4 wave64s owns 128 train rows or 128 test rows of one
-//    (b, h); 32 per wave; test rows may attend to a shared K/V head;
+//  * a workgroup of W wave64s owns 32 W train rows or test rows of one
+//    (b, h); 32 per wave; test rows may attend to a shared K/V head; W = 4,
+//    or 8 at head dimension 128 where that grid still fills the chip (as in
+//    the FP8 kernel; the width changes no output bit);
 //  * fp32 inputs are rounded to bf16 (nearest even) as they are loaded;
 //  * key blocks of kBlockKvBf16 keys; K and V are staged through LDS in their
 //    row-major bf16 layout (double-buffered, one barrier per block);
@@ -25,7 +27,8 @@
 namespace tfm {
 namespace {
 
-constexpr int kRowsPerBlock = 128;
+constexpr int kRowsPerBlock = 128;      // query rows of a 4-wave workgroup
+constexpr int kComputeUnitsBf16 = 256;  // MI355X; the width choice only affects speed
 constexpr int kPadB = 16;        // bytes of LDS row padding
 constexpr int kBlockKvBf16 = 64;
 
@@ -87,13 +90,14 @@ __device__ inline float max_across_halves(float x) {
 }
 
 // Stage one block of K and V (BKV keys x D bf16 each, rows >= N as zero) into registers.
-template <int D, int BKV, typename T>
+template <int D, int BKV, typename T, int NT>
 __device__ inline void stage_load(const T* kb_ptr, const T* vb_ptr, int row_stride, int key0, int N,
                                   u32x4* kr, u32x4* vr) {
-  constexpr int PIECES = BKV * D / 8 / 256;
+  constexpr int PIECES = BKV * D / 8 / NT;
+  static_assert(PIECES * NT == BKV * D / 8, "a key block splits evenly over the threads");
 #pragma unroll
   for (int j = 0; j < PIECES; ++j) {
-    const int i = threadIdx.x + 256 * j;
+    const int i = threadIdx.x + NT * j;
     const int r = i / (D / 8), cc = i % (D / 8);
     const int key = key0 + r;
     const size_t off = (size_t)key * row_stride + cc * 8;
@@ -102,26 +106,27 @@ __device__ inline void stage_load(const T* kb_ptr, const T* vb_ptr, int row_stri
   }
 }
 
-template <int D, int BKV>
+template <int D, int BKV, int NT>
 __device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* kr, const u32x4* vr) {
   constexpr int RS = 2 * D + kPadB;
-  constexpr int PIECES = BKV * D / 8 / 256;
+  constexpr int PIECES = BKV * D / 8 / NT;
 #pragma unroll
   for (int j = 0; j < PIECES; ++j) {
-    const int i = threadIdx.x + 256 * j;
+    const int i = threadIdx.x + NT * j;
     const int off = (i / (D / 8)) * RS + (i % (D / 8)) * 16;
     *reinterpret_cast<u32x4*>(k_lds + off) = kr[j];
     *reinterpret_cast<u32x4*>(v_lds + off) = vr[j];
   }
 }
 
-template <int D, int BKV, typename T, bool OUT_BF16>
-__global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
+template <int D, int BKV, typename T, bool OUT_BF16, int W>
+__global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
+  constexpr int NT = 64 * W;             // threads of the workgroup (W waves of 32 query rows)
   constexpr int RS = 2 * D + kPadB;      // LDS row stride (bytes) of both tiles
   constexpr int TBYTES = BKV * RS;
   constexpr int NS = BKV / 32;           // 32-key score tiles
   constexpr int NQ = BKV / 16;           // 16-key PV chunks
-  constexpr int PIECES = BKV * D / 8 / 256;
+  constexpr int PIECES = BKV * D / 8 / NT;
   __shared__ __attribute__((aligned(16))) uint8_t lds[2 * 2 * TBYTES];
 
   const int bh = blockIdx.x / a.tiles;
@@ -132,7 +137,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   const int ql = lane % 32, half = lane / 32;
   const bool test = tile >= a.tiles_train;
   const int rows = test ? M : N;
-  const int row = (test ? tile - a.tiles_train : tile) * kRowsPerBlock + wave * 32 + ql;
+  const int row = (test ? tile - a.tiles_train : tile) * (32 * W) + wave * 32 + ql;
   const int hkv = test ? h / a.test_group : h;   // the K/V head the rows attend to
 
   // Q fragment: for head_dim chunk j (16 wide) the lane holds d in [16j + 8*half, +8)
@@ -173,15 +178,15 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
   const int vtr_off = ((tg / 2) * 4 + tr) * RS + (16 * (tg % 2) + 4 * tj) * 2;
 
   u32x4 kr[PIECES], vr[PIECES];
-  stage_load<D, BKV, T>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
-  stage_store<D, BKV>(lds, lds + TBYTES, kr, vr);
+  stage_load<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
+  stage_store<D, BKV, NT>(lds, lds + TBYTES, kr, vr);
   __syncthreads();
 
   for (int kb = 0; kb < nblocks; ++kb) {
     const uint8_t* k_lds = lds + (kb & 1) * 2 * TBYTES;
     const uint8_t* v_lds = k_lds + TBYTES;
     const bool more = kb + 1 < nblocks;
-    if (more) stage_load<D, BKV, T>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
+    if (more) stage_load<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
 
     v16f st[NS];
 #pragma unroll
@@ -247,7 +252,7 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
     __builtin_amdgcn_s_setprio(0);
     if (more) {
       uint8_t* nk = lds + ((kb + 1) & 1) * 2 * TBYTES;
-      stage_store<D, BKV>(nk, nk + TBYTES, kr, vr);
+      stage_store<D, BKV, NT>(nk, nk + TBYTES, kr, vr);
     }
     __syncthreads();
   }
@@ -277,14 +282,17 @@ __global__ __launch_bounds__(256, 2) void attn_bf16_kernel(Bf16Args a) {
 }  // namespace
 
 template <typename T>
-static void launch_bf16_typed(int out_bf16, int D, const Bf16Args& a, dim3 grid, hipStream_t s) {
-  dim3 block(256);
+static void launch_bf16_typed(int out_bf16, int D, bool wide, const Bf16Args& a, dim3 grid, hipStream_t s) {
+  const dim3 block(wide ? 512 : 256);
   if (D == 64) {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<64, kBlockKvBf16, T, false, 4>), grid, block, 0, s, a);
+  } else if (wide) {
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, true, 8>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, false, 8>), grid, block, 0, s, a);
   } else {
-    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, false>), grid, block, 0, s, a);
+    if (out_bf16) hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, true, 4>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attn_bf16_kernel<128, kBlockKvBf16, T, false, 4>), grid, block, 0, s, a);
   }
 }
 
@@ -293,15 +301,21 @@ hipError_t launch_attn_bf16(int in_f32, int out_bf16, int B, int H, int D, int N
                             void* o_train, void* o_test, hipStream_t s) {
   Bf16Args a;
   a.B = B; a.H = H; a.N = N; a.M = M;
-  a.tiles_train = (N + kRowsPerBlock - 1) / kRowsPerBlock;
-  a.tiles = a.tiles_train + (M + kRowsPerBlock - 1) / kRowsPerBlock;
+  // At head dimension 128, workgroups of 8 waves (256 rows) share each staged key block when
+  // that grid still gives every CU one and fits the launch limit, as in the FP8 kernel; the
+  // width changes no output bit.
+  const long long wide_blocks = (long long)((N + 255) / 256 + (M + 255) / 256) * B * H;
+  const bool wide = D == 128 && wide_blocks >= kComputeUnitsBf16 && wide_blocks <= kMaxGridBlocks / 2;
+  const int rpb = wide ? 256 : kRowsPerBlock;
+  a.tiles_train = (N + rpb - 1) / rpb;
+  a.tiles = a.tiles_train + (M + rpb - 1) / rpb;
   a.test_group = H / test_kv_heads;
   a.alpha = alpha;
   a.q_train = q_train; a.q_test = q_test; a.k = k; a.v = v;
   a.o_train = o_train; a.o_test = o_test;
   dim3 grid((unsigned)((long)a.tiles * B * H));
-  if (in_f32) launch_bf16_typed<float>(out_bf16, D, a, grid, s);
-  else launch_bf16_typed<uint16_t>(out_bf16, D, a, grid, s);
+  if (in_f32) launch_bf16_typed<float>(out_bf16, D, wide, a, grid, s);
+  else launch_bf16_typed<uint16_t>(out_bf16, D, wide, a, grid, s);
   return hipGetLastError();
 }
 

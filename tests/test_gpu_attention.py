@@ -339,7 +339,8 @@ def bf16_bound(q, k, v, alpha):
 
 
 @pytest.mark.parametrize("name,B,H,D,N,M", [("tiny", 1, 2, 64, 512, 128), ("edge", 1, 2, 64, 65, 3),
-                                            ("edge", 2, 1, 128, 300, 50), ("threshold", 1, 6, 64, 8192, 2048)])
+                                            ("edge", 2, 1, 128, 300, 50), ("threshold", 1, 6, 64, 8192, 2048),
+                                            ("wide", 1, 8, 128, 8300, 300)])
 def test_bf16_kernel_against_exact_attention(name, B, H, D, N, M):
     w = WORKLOADS.get(name, Workload(name, B=B, H=H, D=D, N=N, M=M, dtype="bf16", seed=N)).with_(dtype="bf16")
     x = generate(w)
@@ -355,6 +356,19 @@ def test_bf16_kernel_against_exact_attention(name, B, H, D, N, M):
                 rms = np.sqrt(np.mean(ref ** 2))
                 err = np.abs(o[b, rows, h] - ref)
                 assert np.all(err <= 1.25 * bnd + 1e-5 * rms), (err / (bnd + 1e-30)).max()
+
+
+def test_bf16_workgroup_width_changes_no_bit():
+    # B*H*ceil(rows/256) = 280: 8-wave workgroups at head dimension 128; a single head is
+    # 35 such workgroups, too few, so it runs 4-wave ones.  A head's outputs depend only on
+    # its own inputs, so the two must agree bit for bit.
+    w = Workload("wide", B=1, H=8, D=128, N=8300, M=300, dtype="bf16", seed=66)
+    g = gpu_inputs(generate(w), torch.bfloat16)
+    a_tr, a_te = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    for h in (0, 5):
+        one = {k: t[:, :, h:h + 1].contiguous() for k, t in g.items()}
+        b_tr, b_te = tfm.tfm_icl_attention_bf16(one["q_train"], one["k"], one["v"], one["q_test"], alpha=w.alpha)
+        assert torch.equal(b_tr[:, :, 0], a_tr[:, :, h]) and torch.equal(b_te[:, :, 0], a_te[:, :, h])
 
 
 def test_bf16_kernel_invariances(thr):
