@@ -103,14 +103,21 @@ def icl_attention_dequantized(qz, alpha, rows_train=None, rows_test=None, test_k
                          q_te, alpha, rows_train, rows_test, test_kv_heads)
 
 
-def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_sum="p8", tie_rel=None):
+def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_sum="p8", tie_rel=None,
+                           scores=None):
     """One head of the fused FP8 kernel, replayed in fp64.
 
     q8 (R,D), k8 (N,D), v8 (N,D) are the e4m3 *values* (decoded codes),
     c = alpha * s_q * s_k * log2(e) is the factor that turns a raw code dot
-    product into a base-2 logit, s_v the V dequantization scale.
+    product into a base-2 logit, s_v the V dequantization scale.  ``scores``
+    (R,N), if given, stands for the code dot products Q_8 K_8^T (by default
+    they are computed exactly), so that the same replay can be run on the
+    scores of a particular FP8 dot-product arithmetic.  Before the first key
+    block the state is empty; its rescale factor is 0 (as 2^(c (-inf)) is for
+    any c > 0, and also when c underflows to 0).
 
-    With ``tie_rel`` set, also returns the sensitivity of the result to
+    With ``tie_rel`` set (a scalar, or one value per row), also returns the
+    sensitivity of the result to
     rounding ties of P: for every P~ whose e4m3 rounding changes when P~ moves
     by a relative tie_rel, the two candidate codes differ by ``spread``; if an
     implementation picks the other one for any such keys, its output moves by
@@ -124,12 +131,19 @@ def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_su
     acc = np.zeros((R, v8.shape[1]))
     tie_l = np.zeros(R)
     tie_acc = np.zeros((R, v8.shape[1]))
+    if tie_rel is not None and np.ndim(tie_rel):
+        tie_rel = np.asarray(tie_rel, dtype=np.float64).reshape(R, 1)
     for j0 in range(0, N, block_kv):
-        s = q8 @ k8[j0:j0 + block_kv].T          # exact: products of e4m3 values
+        if scores is None:
+            s = q8 @ k8[j0:j0 + block_kv].T      # exact: products of e4m3 values
+        else:
+            s = np.asarray(scores[:, j0:j0 + block_kv], dtype=np.float64)
         m_new = np.maximum(m, s.max(axis=1))
         p = np.exp2(c * (s - m_new[:, None]) + P_LIFT_LOG2)   # <= 2^8
         p8 = round_to_e4m3(p) if quantize_p else p
-        r = np.exp2(c * (m - m_new))             # rescale of the old state; 0 at the start
+        # rescale of the old state; the empty state before the first block has none
+        first = np.isneginf(m)
+        r = np.where(first, 0.0, np.exp2(c * (np.where(first, m_new, m) - m_new)))
         l = l * r + (p8 if row_sum == "p8" else p).sum(axis=1)
         acc = acc * r[:, None] + p8 @ v8[j0:j0 + block_kv]
         if tie_rel is not None:
@@ -144,14 +158,17 @@ def one_pass_fp8_attention(q8, k8, v8, c, s_v, block_kv, quantize_p=True, row_su
 
 
 def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_test=None,
-                                   quantize_p=True, row_sum="p8", tie_rel=None, test_kv_heads=None):
+                                   quantize_p=True, row_sum="p8", tie_rel=None, test_kv_heads=None,
+                                   score_fn=None):
     """O_qp: both ICL calls through ``one_pass_fp8_attention`` for every (b, h).
 
     ``qz`` is the output of ``quantize_qkv_per_head``.  The test call of head
     h uses the test-query scale s_q_test and the codes and scales of K/V head
     ``grouped_kv_head(h, H, test_kv_heads)``.  Returns (o_train, o_test) as
     (B, R, H, D) fp64 for the selected rows; with ``tie_rel`` set, returns
-    ((o_train, allowance_train), (o_test, allowance_test)).
+    ((o_train, allowance_train), (o_test, allowance_test)).  ``score_fn``,
+    if given, maps (query codes (R,D), key codes (N,D)) to the scores the
+    replay uses in place of the exact Q_8 K_8^T.
     """
     B, H, N, D = qz["k8"].shape
     rt = _pick(rows_train, N)
@@ -173,7 +190,8 @@ def icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train=None, rows_te
                 c = float(alpha) * float(s_query) * float(qz["s_k"][b, hkv]) * LOG2E
                 args = (decode(qz["k8"][b, hkv]), decode(qz["v8"][b, hkv]), c, qz["s_v"][b, hkv], block_kv,
                         quantize_p, row_sum, tie_rel)
-                res = one_pass_fp8_attention(decode(qz[key][b, h, rows]), *args)
+                sc = None if score_fn is None else score_fn(qz[key][b, h, rows], qz["k8"][b, hkv])
+                res = one_pass_fp8_attention(decode(qz[key][b, h, rows]), *args, scores=sc)
                 if tie_rel is None:
                     o[b, :, h] = res
                 else:

@@ -71,8 +71,13 @@ MUTATIONS = {
                             "every head dequantized with head 0's scale"),
     "kernel_lift_2_7": ("oracle.attention", "one_pass_fp8_attention", "+ P_LIFT_LOG2)", "+ P_LIFT_LOG2 - 1)",
                         "row maximum lifted to 2^7"),
-    "kernel_no_rescale": ("oracle.attention", "one_pass_fp8_attention", "r = np.exp2(c * (m - m_new))",
-                          "r = np.where(np.isfinite(m), 1.0, 0.0)", "state not rescaled when the max grows"),
+    "kernel_no_rescale": ("oracle.attention", "one_pass_fp8_attention",
+                          "np.exp2(c * (np.where(first, m_new, m) - m_new))", "1.0",
+                          "state not rescaled when the max grows"),
+    "kernel_first_block_rescale": ("oracle.attention", "one_pass_fp8_attention",
+                                   "r = np.where(first, 0.0, np.exp2(c * (np.where(first, m_new, m) - m_new)))",
+                                   "r = np.exp2(c * (m - m_new))",
+                                   "the empty state rescaled by 2^(c (-inf)), NaN when c is 0"),
     "kernel_max_over_rows": ("oracle.attention", "one_pass_fp8_attention",
                              "m_new = np.maximum(m, s.max(axis=1))", "m_new = np.maximum(m, s.max())",
                              "one running max shared by all rows"),

@@ -268,3 +268,37 @@ def test_kernel_model_uses_the_test_query_scale(mode, test_mult):
     # and O_q and O_qp stay within the FP8 quantization error of the exact result on both calls
     for got, ex in ((d_tr, ex_tr), (d_te, ex_te), (o_tr, ex_tr), (o_te, ex_te)):
         assert np.linalg.norm(got - ex) / np.linalg.norm(ex) < 0.1      # a wrong query scale gives ~1
+
+
+def test_kernel_model_with_a_vanishing_softmax_factor_returns_the_mean_of_v():
+    # c = 0 (alpha s_q s_k underflowing): every logit is 0, Eq. (1) gives the plain mean of V,
+    # and the replay must not rescale its empty first state by 2^(0 * -inf)
+    rng = np.random.default_rng(27)
+    N, D = 300, 64
+    q8 = decode(encode_rne(np.clip(rng.standard_normal((7, D)) * 60, -448, 448)))
+    k8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    v8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    for c in (0.0, 1e-300):
+        o = A.one_pass_fp8_attention(q8, k8, v8, c, 0.25, 128)
+        assert np.allclose(o, 0.25 * v8.mean(axis=0), rtol=0, atol=1e-12 * np.abs(v8).max())
+
+
+def test_kernel_model_scores_hook_and_per_row_tie_windows():
+    # scores given explicitly stand for Q_8 K_8^T: the exact products reproduce the default,
+    # and scores doubled with c halved give the same logits, hence the same output
+    rng = np.random.default_rng(28)
+    N, D = 400, 64
+    q8 = decode(encode_rne(np.clip(rng.standard_normal((6, D)) * 60, -448, 448)))
+    k8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    v8 = decode(encode_rne(np.clip(rng.standard_normal((N, D)) * 60, -448, 448)))
+    c = 3e-4
+    base = A.one_pass_fp8_attention(q8, k8, v8, c, 0.5, 128)
+    assert np.array_equal(A.one_pass_fp8_attention(q8, k8, v8, c, 0.5, 128, scores=q8 @ k8.T), base)
+    assert np.allclose(A.one_pass_fp8_attention(q8, k8, v8, c / 2, 0.5, 128, scores=2 * (q8 @ k8.T)), base,
+                       rtol=1e-13, atol=1e-13 * np.abs(base).max())
+    moved = A.one_pass_fp8_attention(q8, k8, v8, c, 0.5, 128, scores=q8 @ k8.T + 1500.0 * (np.arange(N) == 5))
+    assert not np.allclose(moved, base)
+    # a tie window given per row equals the scalar one on every row
+    _, a1 = A.one_pass_fp8_attention(q8, k8, v8, c, 0.5, 128, tie_rel=1e-3)
+    _, a2 = A.one_pass_fp8_attention(q8, k8, v8, c, 0.5, 128, tie_rel=np.full(6, 1e-3))
+    assert np.array_equal(a1, a2)
