@@ -149,7 +149,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
     for (int j = 0; j < D / 16; ++j)
       qf[j] = qrow ? as_bf(load8_as_bf16(qrow + 16 * j + 8 * half)) : as_bf(u32x4{0u, 0u, 0u, 0u});
   }
-  const float c = a.alpha * kLog2e;
+  const float c = fmaxf(a.alpha * kLog2e, kMinNormal);   // as in the FP8 kernel: never 0
 
   // constant operand of the row-sum MFMA: 1.0 in rows {0,8} for k-groups {0,2}
   // and rows {4,12} for k-groups {1,3} (the lanes of one query in the P operand)

@@ -224,7 +224,11 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
 #pragma unroll
     for (int s = 0; s < KD; ++s) qf[s] = qrow ? load32(qrow + 64 * s + 32 * half) : v8i{0, 0, 0, 0, 0, 0, 0, 0};
   }
-  const float c = a.alpha * (test ? a.s_q_test[bh] : a.s_q[bh]) * a.s_k[bhkv] * kLog2e;
+  // A factor below the smallest normal fp32 (alpha s_q s_k underflowing) is taken as that
+  // value: every lifted weight still rounds to exactly 2^8 (|c (S - m)| < 2^-100), as at
+  // c = 0, while masked keys (S = -inf) and the empty first state keep weight 0 instead of
+  // 0 * -inf = NaN.
+  const float c = fmaxf(a.alpha * (test ? a.s_q_test[bh] : a.s_q[bh]) * a.s_k[bhkv] * kLog2e, kMinNormal);
   const float sv = a.s_v[bhkv];
 
   // constant operand of the row-sum MFMA (see the header comment)
@@ -300,7 +304,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
       for (int r = (t == 0 ? 1 : 0); r < 16; ++r) mx = fmaxf(mx, st[t][r]);
     mx = max_across_halves(mx);
     const float m_new = fmaxf(m_run, mx);
-    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 1 where unchanged, 0 at the start
+    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 1 where unchanged, 0 at the start (c > 0)
     const float bias = 8.0f - c * m_new;                                   // lifts the running max to 2^8
     m_run = m_new;
 

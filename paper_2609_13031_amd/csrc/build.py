@@ -44,6 +44,19 @@ def _run(cmd):
     return msg
 
 
+# Test-only GPU code (not part of libtfm): the matrix-instruction probe that the
+# precision tests drive.
+PROBE_SRC = os.path.join(ROOT, "tests", "mfma_probe.hip")
+PROBE_OUT = os.path.join(ROOT, "tests", "libmfma_probe.so")
+
+
+def build_probe():
+    tmp = PROBE_OUT + ".tmp"
+    _run([hipcc(), *FLAGS, "-shared", PROBE_SRC, "-o", tmp])
+    os.replace(tmp, PROBE_OUT)
+    return PROBE_OUT
+
+
 def build(verbose=False):
     os.makedirs(BUILD_DIR, exist_ok=True)
     cc = hipcc()

@@ -22,6 +22,7 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 #endif
 constexpr int kBlockKv = TFM_FP8_BLOCK_KV;  // keys per block (running-max granularity) of the FP8 kernel
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kMinNormal = 1.17549435e-38f;   // smallest normal fp32
 // Which of the two ICL calls an attention launch runs (a mask).
 constexpr int kCallTrain = 1, kCallTest = 2;
 // Most workgroups of 256 threads in one grid dimension: a dispatch holds fewer than

@@ -1,21 +1,23 @@
 """GPU parity of the FP8 and bf16 ICL attention entry points with the oracle.
 
-FP8: against O_qp (the oracle's one-pass kernel model) within T1 and against
-O_q (Eq. (1) on the dequantized inputs) within the e4m3 P-rounding bound T2,
-on every workload (full-size ones on sampled rows: each output row depends
-only on its query and all keys, so a sampled row is checked exactly), plus
-edge shapes, closed forms and invariances.  bf16: against Eq. (1) in fp64."""
+FP8 (tests/parity.py): every checked row elementwise against the oracle's
+one-pass replay fed the FP8 MFMA's measured dot products (T1hw) and against
+Eq. (1) on the dequantized inputs O_q within the derived bound (T2'); in the
+regime where every FP8 dot product is exact, against the oracle's exact replay
+O_qp within fp32 rounding (T1).  Full-size workloads are checked on sampled
+rows: each output row depends only on its own query and all keys, so a
+sampled row is checked exactly.  Plus edge shapes, closed forms and
+invariances.  bf16: against Eq. (1) in fp64 (``oracle.attention``)."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import attention as OA
 from oracle import quantize as OQ
-from oracle.e4m3 import decode
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import WORKLOADS, Workload, generate
-from parity import (EPS_ACC, EPS_DOT, TIE_REL, assert_t1, assert_t1p, assert_t1p_or_t2, assert_t2, gpu_inputs, narrow_range_inputs,
-                    sample_rows)
+from parity import (TIE_REL, assert_t1, bf16_check, check_fp8_call, check_fp8_rows, gpu_inputs, narrow_range_inputs,
+                    pv_rowsum_term, sample_rows)
 
 pytestmark = pytest.mark.gpu
 BKV = 128   # keys per block of the FP8 kernel: the running-max granularity the oracle replays
@@ -41,28 +43,14 @@ def run_workload(w):
     return o_tr, o_te, OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
 
 
-def check_workload(w, rows_tr=None, rows_te=None, t2_rows=None, run=None, heads=None):
-    """T1'/T2' on the selected rows of heads [h0, h1) (default all) of every table."""
+def check_workload(w, rows_tr=None, rows_te=None, run=None, heads=None, t1hw_every=1):
+    """T2' on the selected rows (default all) of the selected heads (default all) of every
+    table, T1hw on every t1hw_every-th of them."""
     o_tr, o_te, qz = run_workload(w) if run is None else run
-    h0, h1 = (0, w.H) if heads is None else heads
-    qz = {k: v[:, h0:h1] for k, v in qz.items()}     # codes (B,H,S,D), scales (B,H)
-    o_tr, o_te = o_tr[:, :, h0:h1], o_te[:, :, h0:h1]
-    r_tr, r_te = OA.icl_attention_fp8_kernel_model(qz, w.alpha, BKV, rows_tr, rows_te)
-    rt = np.arange(w.N) if rows_tr is None else rows_tr
-    re = np.arange(w.M) if rows_te is None else rows_te
-    worst = 0.0
-    for b in range(w.B):
-        for h in range(h1 - h0):
-            for o, r, rows, q8 in ((o_tr, r_tr, rt, qz["q8_train"]), (o_te, r_te, re, qz.get("q8_test"))):
-                if len(rows) == 0:
-                    continue
-                m, t1 = assert_t1p_or_t2(o[b, rows, h], r[b, :, h], qz, w.alpha, b, h, q8[b, h, rows],
-                                         what=(b, h0 + h, len(rows)), t2_max_rows=None if t2_rows is None else 2 * t2_rows)
-                if t1:   # otherwise T2' has just been checked on every row
-                    worst = max(worst, m["relF"])
-                    sub = rows if t2_rows is None else rows[:t2_rows]
-                    assert_t2(o[b, sub, h], qz, w.alpha, b, h, q8[b, h, sub])
-    print("worst relF vs O_qp: %.3e" % worst)
+    m = check_fp8_call((o_tr, o_te), qz, w.alpha, rows_tr, rows_te, block_kv=BKV, what=w.name, heads=heads,
+                       t1hw_every=t1hw_every)
+    print("worst:", m, flush=True)
+    return m
 
 
 @pytest.mark.parametrize("B,H,D,N,M", [(1, 2, 64, 512, 128), (2, 3, 64, 1000, 77), (1, 2, 128, 700, 64)])
@@ -81,7 +69,7 @@ def test_exact_mfma_regime_matches_kernel_model_tightly(B, H, D, N, M):
         for h in range(H):
             m1 = assert_t1(o_tr[b, :, h], r_tr[b, :, h], a_tr[b, :, h], ("train", b, h))
             m2 = assert_t1(o_te[b, :, h], r_te[b, :, h], a_te[b, :, h], ("test", b, h))
-            assert_t2(o_tr[b, :, h], qz, np.float32(alpha), b, h, qz["q8_train"][b, h], eps_dot=0.0)
+    check_fp8_call((o_tr, o_te), qz, np.float32(alpha), None, None, block_kv=BKV, what="narrow")
     print("T1 metrics (last head):", m1, m2)
 
 
@@ -91,17 +79,24 @@ def test_tiny_full():
 
 def test_threshold_sampled():
     w = WORKLOADS["threshold"]
-    check_workload(w, sample_rows(w.N, 256, 1), sample_rows(w.M, 128, 2), t2_rows=64)
+    check_workload(w, sample_rows(w.N, 1024, 1), sample_rows(w.M, 512, 2))
 
 
 def test_many_tables_sampled():
     w = WORKLOADS["many_tables"]
-    check_workload(w, sample_rows(w.N, 48, 3), sample_rows(w.M, 24, 4), t2_rows=16)
+    check_workload(w, sample_rows(w.N, 64, 3), sample_rows(w.M, 32, 4))
 
 
+def mid_rows(w):
+    # 2048 sampled train rows and 512 test rows per head, plus train rows 0..1023 (the rows
+    # the benchmark's accuracy report uses)
+    return np.union1d(sample_rows(w.N, 2048, 5), np.arange(1024)), sample_rows(w.M, 512, 6)
+
+
+@pytest.mark.timeout(900)
 def test_mid_full_size_sampled():
     w = WORKLOADS["mid"]
-    check_workload(w, sample_rows(w.N, 2048, 5), sample_rows(w.M, 512, 6), t2_rows=8)
+    check_workload(w, *mid_rows(w), t1hw_every=2)
 
 
 @pytest.fixture(scope="module")
@@ -109,10 +104,12 @@ def large_run():
     return run_workload(WORKLOADS["large"])
 
 
-@pytest.mark.parametrize("heads", [(0, 4), (4, 8)])
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("heads", [(0, 2), (2, 4), (4, 6), (6, 8)])
 def test_large_full_size_sampled(large_run, heads):
     w = WORKLOADS["large"]
-    check_workload(w, sample_rows(w.N, 2048, 7), sample_rows(w.M, 512, 8), t2_rows=4, run=large_run, heads=heads)
+    check_workload(w, sample_rows(w.N, 2048, 7), sample_rows(w.M, 512, 8), run=large_run, heads=range(*heads),
+                   t1hw_every=8)
 
 
 @pytest.mark.parametrize("name", ["mid", "large"])
@@ -141,7 +138,8 @@ def test_full_size_every_row(name):
     v_hat = OA.dequantize(OQ.quantize_with_scale(x["v"], s_v), s_v)          # (B, N, H, D)
     lo, hi = v_hat.min(axis=1), v_hat.max(axis=1)                            # (B, H, D)
     del v_hat
-    slack = (2 * EPS_DOT + ((w.N + 63) // 64) * EPS_ACC) * 2 * np.maximum(np.abs(lo), np.abs(hi))
+    vmax = np.maximum(np.abs(lo), np.abs(hi)).reshape(-1, w.D)
+    slack = np.stack([pv_rowsum_term(vm, vm[None], w.N)[0] for vm in vmax]).reshape(lo.shape)
     lo = torch.from_numpy(lo - slack).float().cuda()[:, None]
     hi = torch.from_numpy(hi + slack).float().cuda()[:, None]
     for o in (a_tr, a_te):
@@ -153,14 +151,14 @@ def test_d128_wide_workgroups_ragged_rows():
     # B*H*ceil(rows/256) = 280 workgroups: the 8-wave kernel at head dimension 128, with a
     # ragged last key block and partial last query tiles of both calls
     w = Workload("wide", B=1, H=8, D=128, N=8300, M=300, dtype="bf16", seed=64)
-    check_workload(w, sample_rows(w.N, 256, 11), sample_rows(w.M, 64, 12), t2_rows=16)
+    check_workload(w, sample_rows(w.N, 256, 11), sample_rows(w.M, 64, 12))
 
 
 def test_tensors_beyond_4_gib():
     # B*H = 65408 heads of D = 128 and 640 train rows: every train-row tensor holds 5.4 G
     # elements (10.7 GB in bf16, 5.4 GB of codes), so element and byte offsets pass 2^32.
     # Inputs are drawn on the GPU; the heads at the start, the middle and the very end are
-    # checked against the oracle (codes and scales bit for bit, outputs within T1'/T2').
+    # checked against the oracle (codes and scales bit for bit, outputs within T1hw and T2').
     B, H, D, N, M = 511, 128, 128, 640, 64
     gen = torch.Generator(device="cuda").manual_seed(65)
     def draw(rows):
@@ -181,11 +179,8 @@ def test_tensors_beyond_4_gib():
             assert np.array_equal(qz[key][b, h].cpu().numpy(), ref[key][0, 0]), (b, h, key)
         for key in ("s_q", "s_k", "s_v", "s_q_test"):
             assert qz[key][b, h].item() == ref[key][0, 0], (b, h, key)
-        r_tr, r_te = OA.icl_attention_fp8_kernel_model(ref, alpha, BKV)
-        assert_t1p_or_t2(o_tr[b, :, h].cpu().numpy(), r_tr[0, :, 0], ref, alpha, 0, 0, ref["q8_train"][0, 0],
-                         what=(b, h, "train"))
-        assert_t1p_or_t2(o_te[b, :, h].cpu().numpy(), r_te[0, :, 0], ref, alpha, 0, 0, ref["q8_test"][0, 0],
-                         s_query=ref["s_q_test"][0, 0], what=(b, h, "test"))
+        check_fp8_call((o_tr[b:b + 1, :, h:h + 1].cpu().numpy(), o_te[b:b + 1, :, h:h + 1].cpu().numpy()), ref,
+                       alpha, None, None, block_kv=BKV, what=(b, h))
     # the prequantized entry point (public code layout, V re-laid into tiles) gives every row bit for bit
     p_tr, p_te = tfm.tfm_icl_attention_fp8_prequantized(qz["q8_train"], qz["k8"], qz["v8"], qz["q8_test"], qz["s_q"],
                                                         qz["s_k"], qz["s_v"], alpha=float(alpha))
@@ -197,9 +192,7 @@ def test_tensors_beyond_4_gib():
     for b, h in ((0, 0), (510, 127)):
         k, v = (g[n][b, :, h].double().cpu().numpy() for n in ("k", "v"))
         for o, q in ((b_tr, g["q_train"]), (b_te, g["q_test"])):
-            ref, bnd = bf16_bound(q[b, :, h].double().cpu().numpy(), k, v, float(alpha))
-            err = np.abs(o[b, :, h].double().cpu().numpy() - ref)
-            assert np.all(err <= 1.25 * bnd + 1e-5 * np.sqrt(np.mean(ref ** 2))), (b, h)
+            bf16_check(o[b, :, h].cpu().numpy(), q[b, :, h].double().cpu().numpy(), k, v, float(alpha), what=(b, h))
     del g, b_tr, b_te
     torch.cuda.empty_cache()
 
@@ -224,15 +217,39 @@ def test_identical_keys_give_mean_of_v_and_constant_v_is_returned():
     qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
     v_hat = OA.dequantize(qz["v8"], qz["s_v"])
     mean_v = v_hat.mean(axis=1)                                          # (B, H, D)
-    # every lifted weight is exactly 2^8; only the FP8 MFMA accumulation of P V and of l errs
-    rel = 2 * EPS_DOT + ((N + 63) // 64) * EPS_ACC
-    for o in (o_tr, o_te):
-        assert np.all(np.abs(o - mean_v[:, None]) <= rel * (np.abs(v_hat).mean(axis=1)[:, None] + np.abs(mean_v[:, None])))
+    # every lifted weight is exactly 2^8; only the FP8 MFMA arithmetic of P V and of l errs
+    for h in range(H):
+        tol = pv_rowsum_term(np.abs(v_hat[0, :, h]).max(axis=0), mean_v[:, h], N)
+        for o in (o_tr, o_te):
+            assert np.all(np.abs(o[0, :, h] - mean_v[0, h]) <= tol), h
     x["v"] = np.full_like(v, 1.75)
     x["k"] = rng.standard_normal((B, N, H, D)).astype(np.float32) * 4
     o_tr, o_te = fp8(gpu_inputs(x, torch.float32), w)
+    tol = pv_rowsum_term(np.full(D, 1.75), np.full((1, D), 1.75), N)
     for o in (o_tr, o_te):
-        assert np.allclose(o, 1.75, rtol=2 * rel, atol=0)
+        assert np.all(np.abs(o - 1.75) <= tol)
+
+
+def test_vanishing_softmax_factor_gives_the_mean_of_v():
+    # |Q|, |K| ~ 1e-21: s_q s_k underflows, so the kernel's factor c = alpha s_q s_k log2(e)
+    # is 0 in fp32 and every lifted weight is 2^8: the output is the mean of V-hat (Eq. (1)
+    # with logits that are all 0).  The empty state before the first key block is not
+    # rescaled by 2^(0 * -inf).
+    rng = np.random.default_rng(26)
+    B, N, H, D, M = 1, 300, 2, 64, 20
+    q = (rng.standard_normal((B, N + M, H, D)) * 1e-21).astype(np.float32)
+    k = (rng.standard_normal((B, N, H, D)) * 1e-21).astype(np.float32)
+    v = rng.standard_normal((B, N, H, D)).astype(np.float32)
+    x = {"q_train": q[:, :N].copy(), "k": k, "v": v, "q_test": q[:, N:].copy()}
+    o_tr, o_te = fp8(gpu_inputs(x, torch.float32), Workload("tiny_c", B=B, H=H, D=D, N=N, M=M, dtype="f32"))
+    qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
+    assert np.float32(np.float32(1 / 8) * qz["s_q"][0, 0] * qz["s_k"][0, 0]) == 0
+    mean_v = OA.dequantize(qz["v8"], qz["s_v"]).mean(axis=1)
+    for h in range(H):
+        tol = pv_rowsum_term(np.abs(OA.dequantize(qz["v8"], qz["s_v"])[0, :, h]).max(axis=0), mean_v[:, h], N)
+        for o in (o_tr, o_te):
+            assert np.all(np.isfinite(o))
+            assert np.all(np.abs(o[0, :, h] - mean_v[0, h]) <= tol), h
 
 
 def test_one_hot_rows():
@@ -317,26 +334,14 @@ def test_train_row_permutation(thr):
     qz = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"])
     pc = perm.cpu().numpy()
     rows = sample_rows(w.N, 32, 24)
-    for b in range(w.B):
-        for h in range(w.H):
-            assert_t2(b_tr[b, rows, h], qz, w.alpha, b, h, qz["q8_train"][b, h, pc[rows]])
-            assert_t2(b_te[b, :32, h], qz, w.alpha, b, h, qz["q8_test"][b, h, :32])
+    # the permuted call's rows are the original rows pc[rows] attending to permuted keys: T2'
+    # against O_q of the original rows (Eq. (1) does not depend on the key order)
+    qzp = {"q8_train": qz["q8_train"][:, :, pc], "k8": qz["k8"][:, :, pc], "v8": qz["v8"][:, :, pc],
+           "q8_test": qz["q8_test"], "s_q": qz["s_q"], "s_k": qz["s_k"], "s_v": qz["s_v"], "s_q_test": qz["s_q_test"]}
+    check_fp8_call((b_tr, b_te), qzp, w.alpha, rows, np.arange(32), block_kv=BKV, what="permuted")
 
 
 # ---------------- bf16 baseline ----------------
-
-def bf16_bound(q, k, v, alpha):
-    """Elementwise bound on |O_bf16 - O| from rounding P to bf16 for the PV product.
-
-    The kernel normalises by the sum of the rounded weights w_j (a row-sum
-    MFMA over the same bf16 P), so O_bf16 - O = sum_j (w_j - p_j)(v_j - O) / sum_j w_j
-    with |w_j - p_j| <= 2^-8 p_j (half a bf16 ulp)."""
-    s = alpha * (q @ k.T)
-    p = np.exp(s - s.max(axis=1, keepdims=True))
-    o = (p @ v) / p.sum(axis=1, keepdims=True)
-    num = np.stack([np.einsum("rj,rj->r", p, np.abs(v[None, :, c] - o[:, c][:, None])) for c in range(v.shape[1])], 1)
-    return o, 2.0 ** -8 * num / ((1 - 2.0 ** -8) * p.sum(axis=1))[:, None]
-
 
 @pytest.mark.parametrize("name,B,H,D,N,M", [("tiny", 1, 2, 64, 512, 128), ("edge", 1, 2, 64, 65, 3),
                                             ("edge", 2, 1, 128, 300, 50), ("threshold", 1, 6, 64, 8192, 2048),
@@ -351,11 +356,8 @@ def test_bf16_kernel_against_exact_attention(name, B, H, D, N, M):
     for b in range(w.B):
         for h in range(w.H):
             for o, q, rows in ((o_tr, x["q_train"], rt), (o_te, x["q_test"], re)):
-                ref, bnd = bf16_bound(q[b, rows, h].astype(np.float64), x["k"][b, :, h].astype(np.float64),
-                                      x["v"][b, :, h].astype(np.float64), w.alpha)
-                rms = np.sqrt(np.mean(ref ** 2))
-                err = np.abs(o[b, rows, h] - ref)
-                assert np.all(err <= 1.25 * bnd + 1e-5 * rms), (err / (bnd + 1e-30)).max()
+                bf16_check(o[b, rows, h], q[b, rows, h].astype(np.float64), x["k"][b, :, h].astype(np.float64),
+                           x["v"][b, :, h].astype(np.float64), w.alpha, what=(name, b, h))
 
 
 def test_bf16_workgroup_width_changes_no_bit():

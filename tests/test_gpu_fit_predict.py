@@ -11,7 +11,7 @@ from oracle import attention as OA
 from oracle import quantize as OQ
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import Workload, generate
-from parity import assert_t1p_or_t2, assert_t2, gpu_inputs
+from parity import check_fp8_call, gpu_inputs, sample_rows
 
 pytestmark = pytest.mark.gpu
 BKV = 128
@@ -77,13 +77,22 @@ def test_per_call_predict_follows_the_oracle(table):
     o_te = tfm.tfm_icl_attention_fp8_predict(ws, gq, w.N, alpha=w.alpha, q_scale_mode="per_call").cpu().numpy()
     xr = {k: torch.from_numpy(v).to(torch.bfloat16).float().numpy() for k, v in x.items()}
     qz = OQ.quantize_qkv_per_head(xr["q_train"], xr["k"], xr["v"], gq.float().cpu().numpy(), q_scale_mode="per_call")
-    r_tr, r_te = OA.icl_attention_fp8_kernel_model(qz, w.alpha, BKV, [], None)
-    for b in range(w.B):
-        for h in range(w.H):
-            _, t1 = assert_t1p_or_t2(o_te[b, :, h], r_te[b, :, h], qz, w.alpha, b, h, qz["q8_test"][b, h],
-                                     s_query=qz["s_q_test"][b, h], what=(b, h))
-            if t1:
-                assert_t2(o_te[b, :40, h], qz, w.alpha, b, h, qz["q8_test"][b, h, :40], s_query=qz["s_q_test"][b, h])
+    check_fp8_call((np.zeros((w.B, 0, w.H, w.D)), o_te), qz, w.alpha, [], None, block_kv=BKV, what="per_call")
+
+
+@pytest.mark.parametrize("G", [0, 1])
+def test_shared_fit_and_predict_follow_the_oracle(table, G):
+    # fit's train rows and a later predict batch, on the shared train-query scale, against
+    # the oracle directly (the fused call they equal is checked elsewhere too)
+    w, x, g = table
+    o_tr, ws = tfm.tfm_icl_attention_fp8_fit(g["q_train"], g["k"], g["v"], alpha=w.alpha, m_max=w.M)
+    rows = np.arange(100, 400)
+    o_te = tfm.tfm_icl_attention_fp8_predict(ws, g["q_test"][:, rows].contiguous(), w.N, alpha=w.alpha,
+                                             test_kv_heads=G)
+    xr = {k: torch.from_numpy(v).to(torch.bfloat16).float().numpy() for k, v in x.items()}
+    qz = OQ.quantize_qkv_per_head(xr["q_train"], xr["k"], xr["v"], xr["q_test"][:, rows])
+    check_fp8_call((o_tr.cpu().numpy(), o_te.cpu().numpy()), qz, w.alpha, sample_rows(w.N, 128, 64), None,
+                   test_kv_heads=G or None, block_kv=BKV, what=("fit/predict", G))
 
 
 def test_fit_predict_edge_cases(table):

@@ -1,6 +1,8 @@
 """GPU parity of tfm_quantize_qkv_per_head with the oracle quantizer (Eq. (2)):
-codes and scales bit-exact, at every workload size, plus every finite bf16
-value against a sweep of scales."""
+codes and scales bit-exact on every element at every workload size, plus every
+finite bf16 value against a sweep of scales."""
+import concurrent.futures as cf
+
 import numpy as np
 import pytest
 import torch
@@ -8,7 +10,7 @@ import torch
 from oracle import quantize as OQ
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import WORKLOADS, Workload, generate
-from parity import gpu_inputs, sample_rows, to_dev
+from parity import gpu_inputs, to_dev, workers
 
 pytestmark = pytest.mark.gpu
 KEYS = ("q8_train", "k8", "v8", "q8_test")
@@ -31,8 +33,11 @@ def test_codes_and_scales_bit_exact_full(name):
         assert np.array_equal(got[k], ref[k]), (name, k, np.count_nonzero(got[k] != ref[k]))
 
 
+@pytest.mark.timeout(900)
 @pytest.mark.parametrize("name", ["mid", "large"])
-def test_codes_and_scales_bit_exact_full_size_sampled_rows(name):
+def test_codes_and_scales_bit_exact_full_size_every_element(name):
+    # every code of every tensor against the oracle's quantizer, one (tensor, head) at a time
+    # on a pool of threads (the oracle is numpy; the slices are independent)
     w = WORKLOADS[name]
     print("generating", name, flush=True)
     x = generate(w)
@@ -42,11 +47,22 @@ def test_codes_and_scales_bit_exact_full_size_sampled_rows(name):
          "s_v": OQ.scale_from_amax(OQ.absmax_per_head(x["v"]))}
     for k in s:
         assert np.array_equal(got[k], s[k]), k
-    rt, re = sample_rows(w.N, 4096, 1), sample_rows(w.M, 1024, 2)
-    for key, src, sc, rows in (("q8_train", "q_train", "s_q", rt), ("k8", "k", "s_k", rt),
-                               ("v8", "v", "s_v", rt), ("q8_test", "q_test", "s_q", re)):
-        ref = OQ.quantize_with_scale(x[src][:, rows], s[sc])
-        assert np.array_equal(got[key][:, :, rows], ref), key
+    jobs = [(key, src, sc, h) for key, src, sc in (("q8_train", "q_train", "s_q"), ("k8", "k", "s_k"),
+                                                    ("v8", "v", "s_v"), ("q8_test", "q_test", "s_q"))
+            for h in range(w.H)]
+
+    def one(job):
+        key, src, sc, h = job
+        ref = OQ.quantize_with_scale(np.ascontiguousarray(x[src][:, :, h:h + 1]), s[sc][:, h:h + 1])
+        return job, int(np.count_nonzero(got[key][:, h:h + 1] != ref)), ref.size
+
+    checked = 0
+    with cf.ThreadPoolExecutor(workers()) as ex:
+        for job, bad, n in ex.map(one, jobs):
+            assert bad == 0, (name, job, bad)
+            checked += n
+    assert checked == (3 * w.N + w.M) * w.B * w.H * w.D
+    print("%s: %d codes bit-exact" % (name, checked), flush=True)
 
 
 BF16_SCALES_AMAX = [1.0, 448.0, 3.0, 0.1, 1e-3, 7.77e5, 2.0 ** -100, 1.5e-38, 3.3e38, 0.0]

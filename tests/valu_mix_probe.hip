@@ -10,7 +10,7 @@
 //
 // Build and run (from the repository root):
 //   hipcc -O3 --offload-arch=gfx950 -Xclang -target-feature -Xclang -packed-fp32-ops \
-//     paper_2609_13031_amd/csrc/valu_mix_probe.hip -o valu_mix_probe && ./valu_mix_probe
+//     tests/valu_mix_probe.hip -o valu_mix_probe && ./valu_mix_probe
 #include <hip/hip_runtime.h>
 #include <cstdint>
 #include <cstdio>
