@@ -109,7 +109,7 @@ def large_run():
 def test_large_full_size_sampled(large_run, heads):
     w = WORKLOADS["large"]
     check_workload(w, sample_rows(w.N, 2048, 7), sample_rows(w.M, 512, 8), run=large_run, heads=range(*heads),
-                   t1hw_every=8)
+                   t1hw_every=16)
 
 
 @pytest.mark.parametrize("name", ["mid", "large"])
