@@ -26,8 +26,10 @@ if ROOT not in sys.path:
 METRIC = "FP8 ICL attention TFLOP/s + speedup vs bf16 at N_train=65536, 1 MI355X"
 FP8_PEAK_TFLOPS = 5000.0          # MI355X dense FP8 MFMA
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
+SQ_COUNTERS = os.path.join(ROOT, "profiles", "attn_mid_sq_counters.txt")
 CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
 HBM_PEAK_GBS = 8000.0
+ORACLE_BLOCK_KV = 128             # key block of the FP8 kernel's running max, checked against the library
 # The FP8 kernel's VALU work per (query, key) score is one v_fma_f32, one v_exp_f32, half a
 # v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (3.29, 8.68, 8.82 and
 # 5.64 cycles per wave64 instruction) over 1024 SIMDs at 2.4 GHz give this many scores per
@@ -49,22 +51,40 @@ def source_digest(name):
     return hashlib.sha256("\n".join(x for x in lines if x).encode()).hexdigest()[:16]
 
 
-def counter_value(key, source):
-    """A figure from the committed rocprofv3 --pmc summary, or None when it is missing
-    or was taken on a different version of the kernel source it measures."""
-    if not os.path.exists(COUNTERS):
+def counter_value(key, source, path=COUNTERS):
+    """A figure from a committed rocprofv3 summary under profiles/, or None when it is
+    missing or was taken on a different version of the kernel source it measures."""
+    if not os.path.exists(path):
         return None
     kv = {}
-    for line in open(COUNTERS):
+    for line in open(path):
         if ":" in line and not line.startswith("#"):
             k, v = line.split(":", 1)
             kv[k.strip()] = v.strip()
     if kv.get(source.replace(".hip", "") + "_source_sha256_16") != source_digest(source):
         return None
     try:
-        return float(kv[key])
-    except (KeyError, ValueError):
+        return float(kv[key].split()[0])
+    except (KeyError, ValueError, IndexError):
         return None
+
+
+def sq_figures(w):
+    """The FP8 attention kernel's SQ/GRBM counter figures on the headline workload, from the
+    committed rocprofv3 summary (None where it is missing or stale): the clock under load,
+    MFMA and VALU busy fractions, the FP8 MFMA FLOP the kernel issues per launch and the rate
+    they imply at the counted duration, and the share of (wave, key block) pairs skipped
+    exactly (their weights all round to e4m3 zero), which issue only the QK^T MFMAs."""
+    if w.name != "mid":
+        return None
+    get = lambda k: counter_value(k, "attn_fp8.hip", SQ_COUNTERS)
+    out = {"clock_ghz": get("fp8_clock_ghz"), "mfma_busy": get("fp8_mfma_busy"), "valu_busy": get("fp8_valu_busy"),
+           "mfma_flop_per_launch": get("fp8_mfma_flop_per_launch"),
+           "mfma_tflops_at_counted_duration": get("fp8_mfma_tflops_at_counted_duration"),
+           "valu_instructions_per_wave_and_key_block": get("fp8_valu_insts_per_wave_block"),
+           "skipped_block_fraction": get("fp8_skipped_block_fraction"),
+           "source": "profiles/attn_mid_sq_counters.txt"}
+    return out if any(v is not None for k, v in out.items() if k != "source") else None
 
 
 def metrics(got, ref):
@@ -84,28 +104,75 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(x, w, rows, block_kv):
-    """The oracle, single-threaded, on a bounded sample of the same workload; also returns
-    its quantized codes and its O_qp rows (table 0, head 0) for the accuracy report."""
+_POOL_INPUTS = {}
+
+
+def _pool_quantize(bh):
+    """Worker: the oracle's Eq. (2) for one (table, head) of the workload."""
     import numpy as np
     from threadpoolctl import threadpool_limits
-    from oracle import attention as OA
     from oracle import quantize as OQ
-
+    x = _POOL_INPUTS["x"]
+    b, h = bh
+    sl = lambda a: np.ascontiguousarray(a[b:b + 1, :, h:h + 1, :])
     with threadpool_limits(limits=1):
-        sl = lambda a: np.ascontiguousarray(a[:1, :, :1, :])          # table 0, head 0
-        t0 = time.perf_counter()
         qz = OQ.quantize_qkv_per_head(sl(x["q_train"]), sl(x["k"]), sl(x["v"]), sl(x["q_test"]))
-        t_quant = time.perf_counter() - t0
+    return bh, qz
+
+
+def _pool_replay(job):
+    """Worker: the oracle's one-pass kernel model on some query rows of one (table, head)."""
+    from threadpoolctl import threadpool_limits
+    from oracle import attention as OA
+    bh, qz, alpha, block_kv, rows_train, rows_test = job
+    with threadpool_limits(limits=1):
+        o_tr, o_te = OA.icl_attention_fp8_kernel_model(qz, alpha, block_kv, rows_train, rows_test)
+    return bh, rows_train, o_tr[0, :, 0]
+
+
+def cpu_baseline(x, w, rows_train, rows_test, block_kv, workers):
+    """The oracle, as it stands, on a bounded sample of the workload, spread over ``workers``
+    processes forked before anything touches the GPU: Eq. (2) for every (table, head), then
+    the one-pass kernel model for rows_train train and rows_test test rows of each.  Returns
+    the report, the oracle's O_qp for train rows [0, accuracy rows) of table 0, head 0, and
+    that head's codes."""
+    import multiprocessing as mp
+    import numpy as np
+    _POOL_INPUTS["x"] = x
+    heads = [(b, h) for b in range(w.B) for h in range(w.H)]
+    ctx = mp.get_context("fork")
+    with ctx.Pool(workers) as pool:
         t0 = time.perf_counter()
-        o_qp, _ = OA.icl_attention_fp8_kernel_model(qz, w.alpha, block_kv, np.arange(rows), [])
+        qzs = dict(pool.map(_pool_quantize, heads))
+        t_quant = time.perf_counter() - t0
+        chunk = 512
+        jobs = [((b, h), qzs[(b, h)], w.alpha, block_kv, np.arange(r0, min(rows_train, r0 + chunk)), [])
+                for (b, h) in heads for r0 in range(0, rows_train, chunk)]
+        jobs += [((b, h), qzs[(b, h)], w.alpha, block_kv, [], np.arange(r0, min(rows_test, r0 + chunk)))
+                 for (b, h) in heads for r0 in range(0, rows_test, chunk)]
+        t0 = time.perf_counter()
+        res = pool.map(_pool_replay, jobs, chunksize=1)
         t_attn = time.perf_counter() - t0
+    _POOL_INPUTS.clear()
+    rows = len(heads) * (rows_train + rows_test)
     flops = 4.0 * w.D * w.N * rows
-    return {"value": flops / t_attn / 1e12, "unit": "TFLOP/s", "cores": 1, "kind": "oracle",
-            "sample": "one-pass FP8 kernel model (fp64 numpy) for %d train query rows of table 0, head 0, "
-                      "against all %d keys; quantization of that head (N+M rows) took %.2f s more" %
-                      (rows, w.N, t_quant),
-            "seconds": round(t_attn, 2), "cpu_model": cpu_model()}, o_qp[0, :, 0], qz
+    head0 = np.concatenate([o for bh, rt, o in res if bh == (0, 0) and len(rt)])
+    report = {"value": round(flops / t_attn / 1e12, 5), "unit": "TFLOP/s", "cores": workers, "kind": "oracle",
+              "sample": "one-pass FP8 kernel model (fp64 numpy) for train rows 0..%d and test rows 0..%d of every "
+                        "one of the %d (table, head) pairs, each against all %d keys, in %d worker processes; "
+                        "Eq. (2) for all of the workload's elements took %.2f s more" %
+                        (rows_train - 1, rows_test - 1, len(heads), w.N, workers, t_quant),
+              "seconds": round(t_attn, 2), "quantize_seconds": round(t_quant, 2), "cpu_model": cpu_model()}
+    return report, head0, qzs[(0, 0)]
+
+
+def cpu_workers():
+    """Processes for the CPU baseline: the host cores this process may run on, at most 16."""
+    try:
+        n = len(os.sched_getaffinity(0))
+    except AttributeError:
+        n = os.cpu_count() or 1
+    return max(1, min(16, n))
 
 
 def accuracy(x, w, o_qp, qz, gpu_fp8, gpu_bf16, rows):
@@ -243,7 +310,10 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mid")
-    ap.add_argument("--cpu-rows", type=int, default=12288, help="query rows of the oracle sample")
+    ap.add_argument("--cpu-train-rows", type=int, default=4096,
+                    help="train query rows per (table, head) of the oracle sample")
+    ap.add_argument("--cpu-test-rows", type=int, default=1024,
+                    help="test query rows per (table, head) of the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--accuracy-rows", type=int, default=1024,
                     help="rows of the oracle sample also compared with fp64 attention (with the CPU baseline)")
@@ -267,20 +337,30 @@ def main():
         sys.exit(2)
 
     import numpy as np
+    from paper_2609_13031_amd.workloads import WORKLOADS, generate
+
+    w = WORKLOADS[args.workload]
+    cpu = None
+    if not (args.crossover or args.noise):
+        log("generating", w)
+        x = generate(w)
+        if not args.no_cpu_baseline:
+            # before anything touches the GPU: the pool's workers are forked from this process
+            n = cpu_workers()
+            log("cpu baseline (oracle) in %d processes" % n)
+            cpu = cpu_baseline(x, w, min(args.cpu_train_rows, w.N), min(args.cpu_test_rows, w.M), ORACLE_BLOCK_KV, n)
+            log("cpu baseline: %s" % cpu[0])
+
     import torch
     from paper_2609_13031_amd import tfm
-    from paper_2609_13031_amd.workloads import WORKLOADS, generate
 
     tfm.lib()
     if args.crossover:
         print(json.dumps(crossover(args.crossover_max_n)), flush=True)
         return
-    w = WORKLOADS[args.workload]
     if args.noise:
         print(json.dumps(noise_op(w, args.steps, args.warmup)), flush=True)
         return
-    log("generating", w)
-    x = generate(w)
     in_dt = torch.float32 if w.dtype == "f32" else torch.bfloat16
     dev = torch.device("cuda:0")
     g = {k: torch.from_numpy(v).to(in_dt).to(dev) for k, v in x.items()}
@@ -382,7 +462,7 @@ def main():
         "torch_sdpa_bf16_context": sdpa,
         "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
-                     "traffic": traffic},
+                     "traffic": traffic, "counters": sq_figures(w)},
         "alu_roofline": {"kernel": "attn_fp8_kernel", "bound": "alu", "achieved": round(achieved, 2),
                          "peak": round(ALU_SCORES_PER_S * 4 * w.D / 1e12, 1), "unit": "TFLOP/s",
                          "frac": round(achieved / (ALU_SCORES_PER_S * 4 * w.D / 1e12), 4),
@@ -392,14 +472,15 @@ def main():
                          "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": round(q_gbs / HBM_PEAK_GBS, 4),
                          "traffic": counter_value("quantize_stage_hbm_bytes_per_step", "quantize.hip")},
     }
-    if not args.no_cpu_baseline:
-        log("cpu baseline (oracle) on %d rows" % args.cpu_rows)
-        bkv = tfm.tfm_icl_attention_fp8_block_kv(w.D)
-        result["cpu_baseline"], o_qp, qz = cpu_baseline(x, w, args.cpu_rows, bkv)
+    if cpu is not None:
+        if tfm.tfm_icl_attention_fp8_block_kv(w.D) != ORACLE_BLOCK_KV:
+            raise RuntimeError("the oracle sample replayed key blocks of %d; the library uses %d"
+                               % (ORACLE_BLOCK_KV, tfm.tfm_icl_attention_fp8_block_kv(w.D)))
+        result["cpu_baseline"], o_qp, qz = cpu
         # one more FP8 call (and bf16 call) with fp32 outputs, outside the timed region
         f_tr, f_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha,
                                                workspace=ws)
-        r = min(args.accuracy_rows, args.cpu_rows)
+        r = min(args.accuracy_rows, len(o_qp))
         gpu_fp8 = f_tr[0, :r, 0].cpu().numpy()
         gpu_bf16 = None
         if not args.no_bf16:
