@@ -195,6 +195,32 @@ int tfm_icl_attention_fp8_attend(int out_dtype, const tfm_icl_options* opts, int
                                  size_t workspace_bytes, tfm_stream stream);
 
 /*
+ * tfm_icl_attention_fp8_noalloc -- tfm_icl_attention_fp8 for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid allocation): the same arguments without a workspace,
+ * the same kernels and the same results bit for bit.  The workspace is the
+ * library's own fixed scratch of TFM_NOALLOC_SCRATCH_BYTES (64 MiB) per GPU,
+ * a device array that each GPU the library runs on holds until the process
+ * ends.  The scratch of the current device is used, so `stream` must belong
+ * to the current device.  Nothing in it needs to start at zero: every call
+ * writes what it later reads.
+ *
+ * Errors: TFM_ERR_WORKSPACE_TOO_SMALL when the call needs more scratch than
+ * that (tfm_icl_attention_fp8_workspace_bytes(B, H, D, N, M) above
+ * TFM_NOALLOC_SCRATCH_BYTES: up to about 64 M codes of Q_train, K, V and
+ * Q_test together, e.g. B = 1, H = 8, D = 64, N = 32768, M = 4096); otherwise
+ * as tfm_icl_attention_fp8.  The entry point calls no allocating routine; its
+ * first call on a device looks up the scratch's device address there.
+ * Calls that overlap on one GPU (different streams, or threads) share the
+ * scratch and race: order them.
+ */
+#define TFM_NOALLOC_SCRATCH_BYTES (64u << 20)
+int tfm_icl_attention_fp8_noalloc(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H,
+                                  int D, int N, int M, float alpha, const void* q_train, const void* k,
+                                  const void* v, const void* q_test, void* o_train, void* o_test,
+                                  tfm_stream stream);
+
+/*
  * tfm_icl_attention_fp8_fit / tfm_icl_attention_fp8_predict -- the two ICL
  * calls split the way a tabular foundation model is used: fit once on the
  * train rows, then predict any number of test batches against the same

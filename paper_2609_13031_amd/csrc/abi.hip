@@ -1,7 +1,9 @@
 // libtfm C ABI: argument validation, workspace layout and launch sequences.
 // The operations and conventions are documented in include/tfm.h.
+#include <atomic>
 #include <climits>
 #include <cmath>
+#include <mutex>
 
 #include "../../include/tfm.h"
 #include "common.h"
@@ -83,6 +85,32 @@ int parse_opts(const tfm_icl_options* o, int H, Opts* out) {
 }
 
 int hip_status(hipError_t e) { return e == hipSuccess ? TFM_OK : TFM_ERR_HIP; }
+
+// Scratch of tfm_icl_attention_fp8_noalloc: one copy per GPU, at its own address on
+// each.  In host code `scratch` only names the symbol; the device address comes
+// from hipGetSymbolAddress, taken once per device (with that device current) and
+// kept in scratch_ptr.
+static __device__ __align__(256) uint8_t scratch[TFM_NOALLOC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+std::atomic<void*> scratch_ptr[kMaxDevices];
+std::mutex scratch_mu;
+
+// The device address of the current device's scratch (set up on the first call there).
+int current_scratch(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return TFM_ERR_HIP;
+  void* p = scratch_ptr[dev].load(std::memory_order_acquire);
+  if (!p) {
+    std::lock_guard<std::mutex> lock(scratch_mu);
+    p = scratch_ptr[dev].load(std::memory_order_acquire);
+    if (!p) {
+      if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return TFM_ERR_HIP;
+      scratch_ptr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *out = p;
+  return TFM_OK;
+}
 
 #define TFM_TRY(expr) do { int st_ = (expr); if (st_ != TFM_OK) return st_; } while (0)
 #define TFM_HIP(expr) do { if ((expr) != hipSuccess) return TFM_ERR_HIP; } while (0)
@@ -214,6 +242,25 @@ int tfm_icl_attention_fp8(int in_dtype, int out_dtype, const tfm_icl_options* op
                                          workspace_bytes, stream));
   return tfm_icl_attention_fp8_attend(out_dtype, opts, B, H, D, N, M, alpha, o_train, o_test, workspace,
                                       workspace_bytes, stream);
+}
+
+int tfm_icl_attention_fp8_noalloc(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D,
+                                  int N, int M, float alpha, const void* q_train, const void* k, const void* v,
+                                  const void* q_test, void* o_train, void* o_test, tfm_stream stream) {
+  TFM_TRY(check_shape(B, H, D, N, M));
+  if (fp8_workspace_layout(B, H, D, N, M).total > TFM_NOALLOC_SCRATCH_BYTES) return TFM_ERR_WORKSPACE_TOO_SMALL;
+  if (in_dtype != TFM_F32 && in_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  if (out_dtype != TFM_F32 && out_dtype != TFM_BF16) return TFM_ERR_BAD_DTYPE;
+  TFM_TRY(check_alpha(alpha));
+  Opts o;
+  TFM_TRY(parse_opts(opts, H, &o));
+  const void* req[] = {q_train, k, v, o_train};
+  const void* tst[] = {q_test, o_test};
+  TFM_TRY(check_io(M > 0, req, 4, tst, 2));
+  void* ws = nullptr;
+  TFM_TRY(current_scratch(&ws));
+  return tfm_icl_attention_fp8(in_dtype, out_dtype, opts, B, H, D, N, M, alpha, q_train, k, v, q_test, o_train,
+                               o_test, ws, TFM_NOALLOC_SCRATCH_BYTES, stream);
 }
 
 int tfm_icl_attention_fp8_fit(int in_dtype, int out_dtype, const tfm_icl_options* opts, int B, int H, int D, int N,

@@ -54,6 +54,7 @@ SIGNATURES = {
     "tfm_icl_attention_workspace_bytes": (_c_size, [_c_int] * 6),
     "tfm_icl_attention": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6
                           + [_c_int, ctypes.POINTER(_c_int), _p, _c_size, _p]),
+    "tfm_icl_attention_fp8_noalloc": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 6 + [_p]),
     "tfm_icl_attention_fp8_fit": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 4 + [_c_float] + [_p] * 5
                                   + [_c_size, _p]),
     "tfm_icl_attention_fp8_predict": (_c_int, [_c_int, _c_int, _o] + [_c_int] * 5 + [_c_float] + [_p] * 3
@@ -222,6 +223,21 @@ def tfm_icl_attention_fp8(q_train, k, v, q_test=None, alpha=None, out_dtype=torc
           B, H, D, N, M, _alpha(alpha, D),
           _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _ptr(ws),
           ws.numel(), _stream())
+    return o_tr, o_te
+
+
+def tfm_icl_attention_fp8_noalloc(q_train, k, v, q_test=None, alpha=None, out_dtype=torch.float32, out=None,
+                                  q_scale_mode="shared", test_kv_heads=0):
+    """tfm_icl_attention_fp8 on the library's fixed scratch (no workspace); the outputs are
+    allocated here unless ``out`` gives them."""
+    B, H, D, N, M, q_test = _qkv_dims(q_train, k, v, q_test)
+    if q_train.dtype not in _DTYPES or out_dtype not in _DTYPES:
+        raise ValueError("inputs and outputs must be float32 or bfloat16")
+    dev = _check_inputs({"q_train": q_train, "k": k, "v": v, "q_test": q_test}, q_train.dtype)
+    o_tr, o_te = _outputs(B, H, D, N, M, out_dtype, dev, out)
+    _call("tfm_icl_attention_fp8_noalloc", _DTYPES[q_train.dtype], _DTYPES[out_dtype],
+          _opts(q_scale_mode, test_kv_heads), B, H, D, N, M, _alpha(alpha, D),
+          _ptr(q_train), _ptr(k), _ptr(v), _ptr(q_test), _ptr(o_tr), _ptr(o_te if M else None), _stream())
     return o_tr, o_te
 
 

@@ -20,7 +20,7 @@ def header_functions():
 def test_library_exports_every_declared_function():
     L = tfm.lib()
     names = header_functions()
-    assert len(names) == 18
+    assert len(names) == 19
     for n in names:
         assert hasattr(L, n), n
     assert set(names) == set(tfm.SIGNATURES)
@@ -195,3 +195,22 @@ def test_fit_and_predict_validation():
     need_m = tfm.tfm_icl_attention_fp8_workspace_bytes(1, 2, 64, 300, 50)
     assert need_m > tfm.tfm_icl_attention_fp8_workspace_bytes(1, 2, 64, 300, 0)
     assert p(nws=need_m - 1) == 6
+
+
+def test_noalloc_validation_before_any_hip_call():
+    # every argument error, and a call needing more than the fixed scratch, is reported
+    # before the entry point looks up its scratch (no GPU here)
+    L = tfm.lib()
+    f = L.tfm_icl_attention_fp8_noalloc
+    p = ctypes.c_void_p(16)
+    args = lambda **kw: [kw.get("ind", 1), kw.get("outd", 1), None, kw.get("B", 1), kw.get("H", 8), kw.get("D", 64),
+                         kw.get("N", 4096), kw.get("M", 512), ctypes.c_float(kw.get("alpha", 0.125)),
+                         p, p, p, kw.get("qt", p), p, kw.get("ot", p), None]
+    assert L.tfm_icl_attention_fp8_workspace_bytes(1, 8, 64, 32768, 4096) <= 64 << 20
+    assert L.tfm_icl_attention_fp8_workspace_bytes(1, 8, 64, 65536, 4096) > 64 << 20
+    assert f(*args(N=65536)) == 6                      # beyond TFM_NOALLOC_SCRATCH_BYTES
+    assert f(*args(D=96)) == 4
+    assert f(*args(ind=5)) == 3
+    assert f(*args(alpha=float("nan"))) == 8
+    assert f(*args(qt=None)) == 1
+    assert f(*args(M=0, qt=None, ot=None, N=0)) == 2
