@@ -31,10 +31,11 @@ CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
 HBM_PEAK_GBS = 8000.0
 ORACLE_BLOCK_KV = 128             # key block of the FP8 kernel's running max, checked against the library
 # The FP8 kernel's VALU work per (query, key) score is one v_fma_f32, one v_exp_f32, half a
-# v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (3.29, 8.68, 8.82 and
-# 5.64 cycles per wave64 instruction) over 1024 SIMDs at 2.4 GHz give this many scores per
-# second at most, i.e. 4*D times it in FLOP/s.
-ALU_SCORES_PER_S = 1024 * 2.4e9 * 64 / (3.29 + 8.68 + 8.82 / 2 + 5.64 / 2)
+# v_cvt_pk_fp8_f32 and half a v_max3_f32.  Their measured issue costs (2.96, 8.41, 9.94 and
+# 5.73 cycles per wave64 instruction, counted in cycles of the shader clock each run got) over
+# 1024 SIMDs at the 2.4 GHz peak clock give this many scores per second at most, i.e. 4*D
+# times it in FLOP/s.
+ALU_SCORES_PER_S = 1024 * 2.4e9 * 64 / (2.96 + 8.41 + 9.94 / 2 + 5.73 / 2)
 
 
 def log(*a):
