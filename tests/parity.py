@@ -263,6 +263,8 @@ def check_fp8_call(o, qz, alpha, rows_train, rows_test, test_kv_heads=None, bloc
                     continue
                 m = check_fp8_rows(oo[b, rows, h], qz, alpha, b, h, rows, call, test_kv_heads, block_kv,
                                    what, t2=t2, t1hw_every=t1hw_every)
+                if len(rows) >= 1024:   # progress on the long full-size checks
+                    print("checked %s b=%d h=%d %s: %d rows" % (what, b, h, call, len(rows)), flush=True)
                 worst["relF_vs_hw_replay"] = max(worst["relF_vs_hw_replay"], m["vs_hw_replay"]["relF"])
                 worst["max_over_rms_vs_hw_replay"] = max(worst["max_over_rms_vs_hw_replay"],
                                                          m["vs_hw_replay"]["max_over_rms"])
