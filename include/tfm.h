@@ -35,7 +35,9 @@
  *    other.  A pointer whose element count is 0 (q_test / o_test / q8_test
  *    when M == 0) may be NULL.  The library never allocates device memory
  *    and keeps no state between calls (a fit leaves its train state in the
- *    caller's workspace), so calls are thread-safe.
+ *    caller's workspace), so calls are thread-safe; the one exception is
+ *    tfm_icl_attention_fp8_noalloc, whose calls share a fixed per-GPU scratch
+ *    (see there).
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream); no entry point synchronizes.
  *  - Every argument is validated before anything is enqueued; on a

@@ -3,6 +3,8 @@ of include/tfm.h, and rejects bad arguments before enqueuing anything."""
 import ctypes
 import os
 import re
+import shutil
+import subprocess
 
 import pytest
 
@@ -214,3 +216,18 @@ def test_noalloc_validation_before_any_hip_call():
     assert f(*args(alpha=float("nan"))) == 8
     assert f(*args(qt=None)) == 1
     assert f(*args(M=0, qt=None, ot=None, N=0)) == 2
+
+
+@pytest.mark.skipif(shutil.which("gcc") is None, reason="no host C compiler")
+def test_plain_c_client_compiles_links_and_runs(tmp_path):
+    # the header is plain C99 (no C++ or HIP types in the signatures) and the
+    # library links and resolves with the host C toolchain
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    pkg = os.path.join(root, "paper_2609_13031_amd")
+    exe = str(tmp_path / "c_abi_client")
+    cc = ["gcc", "-std=c99", "-Wall", "-Wextra", "-pedantic", "-Werror", "-I" + os.path.join(root, "include"),
+          os.path.join(root, "tests", "c_abi_client.c"), "-L" + pkg, "-ltfm", "-Wl,-rpath," + pkg, "-o", exe]
+    r = subprocess.run(cc, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr
+    r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0 and "all checks passed" in r.stdout, r.stdout + r.stderr
