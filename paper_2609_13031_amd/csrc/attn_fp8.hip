@@ -141,24 +141,40 @@ __device__ inline void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 // then padded LDS rows (row stride RB + kPad).
 // Stage one key block (BKV keys) of K (row-major, rows >= N read as zero) and
 // V^T (BKV/64 tiles of D x 64 bytes, tiles past the end read as zero) into
-// registers, 16 bytes per thread per piece.  FULL: the caller knows the whole
-// block lies below N, so the loads go unpredicated (no per-block compares and
-// zero fills on all but the last block).
-template <int D, int BKV, bool FULL = false>
+// registers, 16 bytes per thread per piece.  In both tensors piece i of a block
+// lies 16 i bytes after the block's start.
+template <int D, int BKV>
 __device__ inline void stage_load(const uint8_t* kbase, const uint8_t* vbase, int kb, int N, int ntiles64,
                                   u32x4* kr, u32x4* vr) {
   constexpr int PIECES = BKV * D / 16 / 256;
 #pragma unroll
   for (int j = 0; j < PIECES; ++j) {
     const int i = threadIdx.x + 256 * j;
-    const int r = i / (D / 16), cc = i % (D / 16);
-    const int key = kb * BKV + r;
-    kr[j] = (FULL || key < N) ? *reinterpret_cast<const u32x4*>(kbase + (size_t)key * D + cc * 16)
-                              : u32x4{0u, 0u, 0u, 0u};
+    const int key = kb * BKV + i / (D / 16);
+    kr[j] = key < N ? *reinterpret_cast<const u32x4*>(kbase + (size_t)kb * BKV * D + i * 16) : u32x4{0u, 0u, 0u, 0u};
     const int t64 = kb * (BKV / 64) + i / (D * 4);          // 64-key tile of this piece
-    vr[j] = (FULL || t64 < ntiles64)
-                ? *reinterpret_cast<const u32x4*>(vbase + (size_t)t64 * D * 64 + (i % (D * 4)) * 16)
-                : u32x4{0u, 0u, 0u, 0u};
+    vr[j] = t64 < ntiles64 ? *reinterpret_cast<const u32x4*>(vbase + (size_t)kb * (BKV / 64) * D * 64 + i * 16)
+                           : u32x4{0u, 0u, 0u, 0u};
+  }
+}
+
+// A key block known to lie wholly below N: buffer loads through scalar resources
+// based at the block (per-block scalar adds), with each lane's pieces at constant
+// offsets, so the block costs no vector address arithmetic.  Every offset is
+// inside the block, well within the resource's range.
+template <int D, int BKV>
+__device__ inline void stage_load_full(const uint8_t* kbase, const uint8_t* vbase, int kb, u32x4* kr, u32x4* vr) {
+  constexpr int PIECES = BKV * D / 16 / 256;
+  constexpr int KB = BKV * D, VB = (BKV / 64) * D * 64;     // bytes of a K and a V^T block
+  constexpr int kRawBufferDword3 = 0x00020000;              // gfx9 untyped buffer: 32-bit data format
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + (size_t)kb * KB), 0, KB, kRawBufferDword3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + (size_t)kb * VB), 0, VB, kRawBufferDword3);
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    kr[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, threadIdx.x * 16, 4096 * j, 0));
+    vr[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, threadIdx.x * 16, 4096 * j, 0));
   }
 }
 
@@ -270,7 +286,7 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
         uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
         stage_dma<D, BKV, W>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
       } else if ((kb + 2) * BKV <= N) {
-        stage_load<D, BKV, true>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
+        stage_load_full<D, BKV>(kbase, vbase, kb + 1, kr, vr);
       } else {
         stage_load<D, BKV>(kbase, vbase, kb + 1, N, ntiles64, kr, vr);
       }
@@ -303,8 +319,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
 #pragma unroll
       for (int r = (t == 0 ? 1 : 0); r < 16; ++r) mx = fmaxf(mx, st[t][r]);
     mx = max_across_halves(mx);
+    const float m_old = m_run;
     const float m_new = fmaxf(m_run, mx);
-    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));   // 1 where unchanged, 0 at the start (c > 0)
     const float bias = 8.0f - c * m_new;                                   // lifts the running max to 2^8
     m_run = m_new;
 
@@ -329,10 +345,12 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
         }
 
       // ---- l += sum P_8 (row-sum MFMA) and O^T += V_8^T P_8^T ----
-      // Rescale the running state only when some row's max grew (rescale is exactly
-      // 1 where it did not).  Written element-wise so the accumulators are scaled in
-      // place inside the wave-uniform branch.
-      if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
+      // Rescale the running state by 2^(c (m_old - m_new)) only when some row's max
+      // grew: the factor is exactly 1 in the rows where it did not, and 0 in the first
+      // block (m_old = -inf, c > 0).  Written element-wise so the accumulators are
+      // scaled in place inside the wave-uniform branch.
+      if (__builtin_amdgcn_ballot_w64(m_new != m_old)) {
+        const float rescale = __builtin_amdgcn_exp2f(c * (m_old - m_new));
 #pragma unroll
         for (int i = 0; i < D / 32; ++i)
 #pragma unroll
