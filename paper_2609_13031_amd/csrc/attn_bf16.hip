@@ -22,6 +22,8 @@
 //  * the row sum l = sum bf16(P) comes from v_mfma_f32_16x16x32_bf16 of a
 //    constant 0/1 operand against the same P operand, so the weights used in
 //    PV are normalised by their own sum.
+#include <climits>
+
 #include "common.h"
 
 namespace tfm {
@@ -106,6 +108,40 @@ __device__ inline void stage_load(const T* kb_ptr, const T* vb_ptr, int row_stri
   }
 }
 
+// A key block known to lie wholly below N: buffer loads from scalar resources based at
+// the block's first key row (per-block scalar adds), with each lane's pieces at byte
+// offsets `off` fixed for the whole launch, so the block costs no vector address
+// arithmetic.  The caller uses it only where the block's BKV rows of row_stride
+// elements span at most INT_MAX bytes, so every offset lies inside the resource.
+template <int D, int BKV, typename T, int NT>
+__device__ inline void stage_load_full(const T* kb_ptr, const T* vb_ptr, int row_stride, int key0, const int* off,
+                                       u32x4* kr, u32x4* vr) {
+  constexpr int PIECES = BKV * D / 8 / NT;
+  constexpr int kRawBufferDword3 = 0x00020000;              // gfx9 untyped buffer: 32-bit data format
+  const int bytes = BKV * row_stride * (int)sizeof(T);
+  const size_t base = (size_t)key0 * row_stride;
+  const __amdgpu_buffer_rsrc_t rk = __builtin_amdgcn_make_buffer_rsrc((void*)(kb_ptr + base), 0, bytes, kRawBufferDword3);
+  const __amdgpu_buffer_rsrc_t rv = __builtin_amdgcn_make_buffer_rsrc((void*)(vb_ptr + base), 0, bytes, kRawBufferDword3);
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    if constexpr (sizeof(T) == 2) {
+      kr[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rk, off[j], 0, 0));
+      vr[j] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rv, off[j], 0, 0));
+    } else {
+      v4f klo = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rk, off[j], 0, 0));
+      v4f khi = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rk, off[j] + 16, 0, 0));
+      v4f vlo = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rv, off[j], 0, 0));
+      v4f vhi = __builtin_bit_cast(v4f, __builtin_amdgcn_raw_buffer_load_b128(rv, off[j] + 16, 0, 0));
+      v8f kx, vx;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { kx[e] = klo[e]; kx[4 + e] = khi[e]; vx[e] = vlo[e]; vx[4 + e] = vhi[e]; }
+      const v8bf ky = __builtin_convertvector(kx, v8bf), vy = __builtin_convertvector(vx, v8bf);
+      __builtin_memcpy(&kr[j], &ky, 16);
+      __builtin_memcpy(&vr[j], &vy, 16);
+    }
+  }
+}
+
 template <int D, int BKV, int NT>
 __device__ inline void stage_store(uint8_t* k_lds, uint8_t* v_lds, const u32x4* kr, const u32x4* vr) {
   constexpr int RS = 2 * D + kPadB;
@@ -178,6 +214,14 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
   const int vtr_off = ((tg / 2) * 4 + tr) * RS + (16 * (tg % 2) + 4 * tj) * 2;
 
   u32x4 kr[PIECES], vr[PIECES];
+  // buffer-load staging of full blocks where a block's byte span fits the 32-bit offsets
+  const bool buf_ok = (long long)BKV * row_stride * (long long)sizeof(T) <= INT_MAX;
+  int piece_off[PIECES];   // byte offset of each of this thread's pieces within a key block
+#pragma unroll
+  for (int j = 0; j < PIECES; ++j) {
+    const int i = threadIdx.x + NT * j;
+    piece_off[j] = buf_ok ? ((i / (D / 8)) * row_stride + (i % (D / 8)) * 8) * (int)sizeof(T) : 0;
+  }
   stage_load<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, 0, N, kr, vr);
   stage_store<D, BKV, NT>(lds, lds + TBYTES, kr, vr);
   __syncthreads();
@@ -186,7 +230,10 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
     const uint8_t* k_lds = lds + (kb & 1) * 2 * TBYTES;
     const uint8_t* v_lds = k_lds + TBYTES;
     const bool more = kb + 1 < nblocks;
-    if (more) stage_load<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
+    if (more) {
+      if (buf_ok && (kb + 2) * BKV <= N) stage_load_full<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, piece_off, kr, vr);
+      else stage_load<D, BKV, T, NT>(kb_ptr, vb_ptr, row_stride, (kb + 1) * BKV, N, kr, vr);
+    }
 
     v16f st[NS];
 #pragma unroll
@@ -214,8 +261,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
 #pragma unroll
       for (int r = (t == 0 ? 1 : 0); r < 16; ++r) mx = fmaxf(mx, st[t][r]);
     mx = max_across_halves(mx);
+    const float m_old = m_run;
     const float m_new = fmaxf(m_run, mx);
-    const float rescale = __builtin_amdgcn_exp2f(c * (m_run - m_new));
     const float bias = -c * m_new;
     m_run = m_new;
 
@@ -230,7 +277,10 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_bf16_kernel(Bf16Args a) {
       pf[q] = __builtin_convertvector(pv, v8bf);
     }
 
-    if (__builtin_amdgcn_ballot_w64(rescale != 1.0f)) {
+    // rescale by 2^(c (m_old - m_new)) only when some row's max grew (exactly 1 in the
+    // rows where it did not, 0 in the first block)
+    if (__builtin_amdgcn_ballot_w64(m_new != m_old)) {
+      const float rescale = __builtin_amdgcn_exp2f(c * (m_old - m_new));
 #pragma unroll
       for (int i = 0; i < D / 32; ++i)
 #pragma unroll
