@@ -200,6 +200,8 @@ def test_tensors_beyond_4_gib():
 @pytest.mark.parametrize("B,H,D,N,M,dtype", [
     (1, 1, 64, 1, 1, "f32"), (1, 2, 64, 63, 0, "bf16"), (2, 1, 64, 64, 5, "f32"), (1, 3, 64, 65, 130, "bf16"),
     (1, 1, 128, 1, 0, "bf16"), (1, 2, 128, 129, 17, "f32"), (3, 2, 128, 200, 255, "bf16"), (1, 1, 64, 1000, 1, "bf16"),
+    # around the first key block staged as a full block (two whole 128-key blocks) and a whole last block
+    (1, 2, 64, 256, 7, "bf16"), (2, 1, 64, 257, 0, "f32"), (1, 1, 64, 384, 129, "bf16"),
 ])
 def test_edge_shapes(B, H, D, N, M, dtype):
     check_workload(Workload("edge", B=B, H=H, D=D, N=N, M=M, dtype=dtype, seed=B * 1000 + N + M))
@@ -358,6 +360,23 @@ def test_bf16_kernel_against_exact_attention(name, B, H, D, N, M):
             for o, q, rows in ((o_tr, x["q_train"], rt), (o_te, x["q_test"], re)):
                 bf16_check(o[b, rows, h], q[b, rows, h].astype(np.float64), x["k"][b, :, h].astype(np.float64),
                            x["v"][b, :, h].astype(np.float64), w.alpha, what=(name, b, h))
+
+
+@pytest.mark.parametrize("B,H,D,N,M", [(1, 2, 64, 257, 33), (2, 1, 128, 300, 0), (1, 3, 64, 1000, 100)])
+def test_bf16_kernel_rounds_fp32_inputs_on_load(B, H, D, N, M):
+    # fp32 inputs are rounded to bf16 (nearest even) as the kernel stages them, so the
+    # reference is Eq. (1) on the bf16-rounded inputs
+    w = Workload("f32in", B=B, H=H, D=D, N=N, M=M, dtype="f32", seed=700 + N)
+    x = generate(w)
+    g = gpu_inputs(x, torch.float32)
+    o_tr, o_te = tfm.tfm_icl_attention_bf16(g["q_train"], g["k"], g["v"], g["q_test"], alpha=w.alpha)
+    o_tr, o_te = o_tr.cpu().numpy(), o_te.cpu().numpy()
+    r = {k: torch.from_numpy(v).to(torch.bfloat16).double().numpy() for k, v in x.items()}
+    for b in range(B):
+        for h in range(H):
+            for o, q in ((o_tr, r["q_train"]), (o_te, r["q_test"])):
+                if q.shape[1]:
+                    bf16_check(o[b, :, h], q[b, :, h], r["k"][b, :, h], r["v"][b, :, h], w.alpha, what=(N, b, h))
 
 
 def test_bf16_workgroup_width_changes_no_bit():
