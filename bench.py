@@ -27,6 +27,7 @@ METRIC = "FP8 ICL attention TFLOP/s + speedup vs bf16 at N_train=65536, 1 MI355X
 FP8_PEAK_TFLOPS = 5000.0          # MI355X dense FP8 MFMA
 COUNTERS = os.path.join(ROOT, "profiles", "attn_fp8_mid_counters.txt")
 SQ_COUNTERS = os.path.join(ROOT, "profiles", "attn_mid_sq_counters.txt")
+CLOCK_LIB = os.path.join(ROOT, "tests", "libclock_sampler.so")   # test-only shader-clock sampler
 CSRC = os.path.join(ROOT, "paper_2609_13031_amd", "csrc")
 HBM_PEAK_GBS = 8000.0
 ORACLE_BLOCK_KV = 128             # key block of the FP8 kernel's running max, checked against the library
@@ -86,6 +87,33 @@ def sq_figures(w):
            "skipped_block_fraction": get("fp8_skipped_block_fraction"),
            "source": "profiles/attn_mid_sq_counters.txt"}
     return out if any(v is not None for k, v in out.items() if k != "source") else None
+
+
+def live_clock(run_steps, window_ms):
+    """The shader clock while run_steps() runs on the current stream: the test-only sampler
+    (one sleeping wave on a second, default-priority stream) reads s_memtime against
+    s_memrealtime over a window of window_ms from the start.  None if the sampler library is
+    not built or the launch fails."""
+    import ctypes
+    import torch
+    if not os.path.exists(CLOCK_LIB):
+        return None
+    L = ctypes.CDLL(CLOCK_LIB)
+    L.clock_sampler_launch.restype = ctypes.c_int
+    L.clock_sampler_launch.argtypes = [ctypes.c_void_p, ctypes.c_ulonglong, ctypes.c_int, ctypes.c_void_p]
+    L.clock_sampler_wall_khz.restype = ctypes.c_int
+    khz = L.clock_sampler_wall_khz()
+    if khz <= 0:
+        return None
+    out = torch.zeros(2, dtype=torch.int64, device="cuda")
+    side = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    if L.clock_sampler_launch(out.data_ptr(), int(window_ms * khz), 1 << 20, side.cuda_stream) != 0:
+        return None
+    run_steps()
+    torch.cuda.synchronize()
+    cycles, ticks = out.cpu().tolist()
+    return cycles / ticks * khz * 1e3 / 1e9 if ticks > 0 else None
 
 
 def metrics(got, ref):
@@ -411,6 +439,14 @@ def main():
     log("fp8 step %.3f ms (quantize %.3f, attention %.3f), wall %.1f ms for %d steps" %
         (ms_step, quant_ms, attn_ms, wall_ms, K))
 
+    # the shader clock over the first 60% of a second, identical run of the K steps
+    def steps():
+        for _ in range(K):
+            quantize()
+            attend()
+    clock_ghz = live_clock(steps, 0.6 * K * ms_step)
+    log("shader clock during the FP8 steps: %s GHz" % clock_ghz)
+
     bf16 = None
     if not args.no_bf16:
         gb = g if in_dt == torch.bfloat16 else {k: v.to(torch.bfloat16) for k, v in g.items()}
@@ -468,7 +504,11 @@ def main():
         "torch_sdpa_bf16_context": sdpa,
         "roofline": {"kernel": "attn_fp8_kernel", "bound": "mfma", "achieved": round(achieved, 2),
                      "peak": FP8_PEAK_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / FP8_PEAK_TFLOPS, 4),
-                     "traffic": traffic, "counters": sq_figures(w)},
+                     "traffic": traffic, "counters": sq_figures(w),
+                     "live_clock": None if clock_ghz is None else {
+                         "shader_ghz": round(clock_ghz, 3), "tflops_per_ghz": round(achieved / clock_ghz, 1),
+                         "how": "s_memtime over s_memrealtime, read by one sleeping wave beside a second run of the "
+                                "timed steps"}},
         "alu_roofline": {"kernel": "attn_fp8_kernel", "bound": "alu", "achieved": round(achieved, 2),
                          "peak": round(ALU_SCORES_PER_S * 4 * w.D / 1e12, 1), "unit": "TFLOP/s",
                          "frac": round(achieved / (ALU_SCORES_PER_S * 4 * w.D / 1e12), 4),

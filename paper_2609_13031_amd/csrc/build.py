@@ -45,16 +45,27 @@ def _run(cmd):
 
 
 # Test-only GPU code (not part of libtfm): the matrix-instruction probe that the
-# precision tests drive.
+# precision tests drive, and the shader-clock sampler the benchmark runs beside the
+# attention kernel.
 PROBE_SRC = os.path.join(ROOT, "tests", "mfma_probe.hip")
 PROBE_OUT = os.path.join(ROOT, "tests", "libmfma_probe.so")
+CLOCK_SRC = os.path.join(ROOT, "tests", "clock_sampler.hip")
+CLOCK_OUT = os.path.join(ROOT, "tests", "libclock_sampler.so")
+
+
+def _build_test_lib(src, out):
+    tmp = out + ".tmp"
+    _run([hipcc(), *FLAGS, "-shared", src, "-o", tmp])
+    os.replace(tmp, out)
+    return out
 
 
 def build_probe():
-    tmp = PROBE_OUT + ".tmp"
-    _run([hipcc(), *FLAGS, "-shared", PROBE_SRC, "-o", tmp])
-    os.replace(tmp, PROBE_OUT)
-    return PROBE_OUT
+    return _build_test_lib(PROBE_SRC, PROBE_OUT)
+
+
+def build_clock_sampler():
+    return _build_test_lib(CLOCK_SRC, CLOCK_OUT)
 
 
 def build(verbose=False):
