@@ -133,6 +133,31 @@ __device__ inline void stage_dma(const uint8_t* kbase, const uint8_t* vbase, int
   }
 }
 
+// A key block known to lie wholly below N, copied into LDS by buffer loads from scalar
+// resources based at the block (per-block scalar adds): each lane's source offsets
+// (voff: the K pieces, then the V pieces, fixed for the launch) and each piece's uniform
+// LDS destination need no vector arithmetic per block.  The offsets are those of
+// stage_dma without the clamp to the last key, which a full block never needs.
+template <int D, int BKV, int W>
+__device__ inline void stage_dma_full(const uint8_t* kbase, const uint8_t* vbase, int kb, const int* voff,
+                                      uint8_t* k_lds, uint8_t* v_lds, int wave) {
+  constexpr int NP = BKV / 64;
+  constexpr int KPIECES = BKV * D / 1024, VPIECES = NP * D * 64 / 1024;
+  constexpr int KB = BKV * D, VB = NP * D * 64;             // bytes of a K and a V^T block
+  constexpr int kRawBufferDword3 = 0x00020000;              // gfx9 untyped buffer: 32-bit data format
+  const __amdgpu_buffer_rsrc_t rk =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(kbase + (size_t)kb * KB), 0, KB, kRawBufferDword3);
+  const __amdgpu_buffer_rsrc_t rv =
+      __builtin_amdgcn_make_buffer_rsrc((void*)(vbase + (size_t)kb * VB), 0, VB, kRawBufferDword3);
+#pragma unroll
+  for (int i = 0; i < KPIECES / W; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rk, (lds_void*)(k_lds + (wave + W * i) * 1024), 16, voff[i], 0, 0, 0);
+#pragma unroll
+  for (int i = 0; i < VPIECES / W; ++i)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rv, (lds_void*)(v_lds + (wave + W * i) * 1024), 16,
+                                             voff[KPIECES / W + i], 0, 0, 0);
+}
+
 // Wait for this wave's outstanding DMA into LDS (vmcnt(0)), before the barrier
 // after which other waves read it.
 __device__ inline void wait_dma() { __builtin_amdgcn_s_waitcnt(0x0F70); }
@@ -268,6 +293,23 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
   const uint8_t* vbase = a.v8t + (size_t)bhkv * ntiles64 * D * 64;
 
   u32x4 kr[kDma ? 1 : PIECES], vr[kDma ? 1 : PIECES];
+  // DMA staging: this lane's byte offsets within a full key block for its pieces (K, then V),
+  // and the wave index as a scalar so that the LDS destinations are scalar too
+  constexpr int KPW = kDma ? BKV * D / 1024 / W : 1, VPW = kDma ? NP * D * 64 / 1024 / W : 1;
+  int dma_off[KPW + VPW];
+  const int wave_s = __builtin_amdgcn_readfirstlane(wave);
+  if constexpr (kDma) {
+#pragma unroll
+    for (int i = 0; i < KPW; ++i) {
+      const int at = (wave_s + W * i) * 1024 + lane * 16, r = at / D, pos = (at % D) >> 4;
+      dma_off[i] = r * D + ((pos ^ swz<D>(r)) << 4);
+    }
+#pragma unroll
+    for (int i = 0; i < VPW; ++i) {
+      const int at = (wave_s + W * i) * 1024 + lane * 16, r = at / 64, pos = (at % 64) >> 4;
+      dma_off[KPW + i] = r * 64 + ((pos ^ swz<64>(r)) << 4);
+    }
+  }
   if constexpr (kDma) {
     stage_dma<D, BKV, W>(kbase, vbase, 0, N, ntiles64, lds, lds + KBYTES, wave, lane);
     wait_dma();
@@ -284,7 +326,8 @@ __global__ __launch_bounds__(64 * W, 8 / W) void attn_fp8_kernel(Fp8Args a) {
     if (more) {
       if constexpr (kDma) {
         uint8_t* nk = lds + ((kb + 1) & 1) * (KBYTES + VBYTES);
-        stage_dma<D, BKV, W>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
+        if ((kb + 2) * BKV <= N) stage_dma_full<D, BKV, W>(kbase, vbase, kb + 1, dma_off, nk, nk + KBYTES, wave_s);
+        else stage_dma<D, BKV, W>(kbase, vbase, kb + 1, N, ntiles64, nk, nk + KBYTES, wave, lane);
       } else if ((kb + 2) * BKV <= N) {
         stage_load_full<D, BKV>(kbase, vbase, kb + 1, kr, vr);
       } else {
