@@ -8,9 +8,11 @@
 //    32 rows; test rows may attend to a shared K/V head (grouped-query
 //    test-train call).  W = 4 at head dimension 64 (three workgroups per CU,
 //    3 waves per SIMD).  At 128, W = 8 (one workgroup per CU, 2 waves per
-//    SIMD: sharing each staged key block among twice the rows measured 7-14%
-//    faster) when that grid still gives every CU a workgroup, else W = 4 (two
-//    per CU).  W changes no output bit: every decision is per wave;
+//    SIMD, each staged key block shared by twice the rows) for long key
+//    streams (N >= 65536) when that grid still gives every CU a workgroup,
+//    else W = 4 (two per CU, whose waves on a SIMD come from different
+//    workgroups and overlap each other's phases).  W changes no output bit:
+//    every decision is per wave;
 //  * keys are processed in blocks of kBlockKv (128), staged through LDS with
 //    double buffering: the global loads of block k+1 are issued before the
 //    math of block k and written to the other buffer after it, one barrier
@@ -41,6 +43,10 @@ namespace {
 
 constexpr int kRowsPerWave = 32;
 constexpr int kComputeUnits = 256;   // MI355X; the wave-count choice below only affects speed
+// Train rows from which 8-wave workgroups pay at head dimension 128 (measured: the
+// 4-wave kernel is 2-11% faster below, level on generic inputs above, and the 8-wave
+// one 14% faster on sharp heads whose blocks are mostly skipped at 262144 rows).
+constexpr int kWideMinTrainRows = 65536;
 constexpr int kPad = 16;  // padded-layout LDS row padding (bytes): conflict-free 16-byte lane reads
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(1))) void global_void;
@@ -457,7 +463,8 @@ hipError_t launch_attn_fp8(int out_bf16, int calls, int B, int H, int D, int N, 
   };
   // (the shape check bounds the 4-wave grid; the 8-wave one, of 512-thread blocks, is used only where it fits too)
   const long long wide_blocks = tiles_of(8 * kRowsPerWave) * B * H;
-  const bool wide = D == 128 && wide_blocks >= kComputeUnits && wide_blocks <= kMaxGridBlocks / 2;
+  const bool wide = D == 128 && N >= kWideMinTrainRows && wide_blocks >= kComputeUnits &&
+                    wide_blocks <= kMaxGridBlocks / 2;
   const int rpb = (wide ? 8 : 4) * kRowsPerWave;
   a.tiles_train = (calls & kCallTrain) ? (N + rpb - 1) / rpb : 0;
   a.tiles = a.tiles_train + ((calls & kCallTest) ? (M + rpb - 1) / rpb : 0);

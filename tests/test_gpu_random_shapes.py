@@ -14,7 +14,7 @@ from oracle import attention as OA
 from oracle import quantize as OQ
 from paper_2609_13031_amd import tfm
 from paper_2609_13031_amd.workloads import Workload, generate
-from parity import check_fp8_call, gpu_inputs
+from parity import check_fp8_call, gpu_inputs, sample_rows
 
 pytestmark = pytest.mark.gpu
 MODES = ("shared", "per_call", "joint")
@@ -56,11 +56,12 @@ def test_random_case(case):
 
 
 def draw_wide_cases(n, seed):
-    """Head dimension 128 with grids of at least 256 workgroups of 256 rows (the 8-wave kernel)."""
+    """Head dimension 128, at least 65536 train rows and grids of at least 256 workgroups of
+    256 rows (the 8-wave kernel)."""
     rng = np.random.default_rng(seed)
     cases = []
     while len(cases) < n:
-        c = dict(B=int(rng.integers(2, 5)), H=int(rng.choice([8, 12, 16])), D=128, N=int(rng.integers(1500, 3200)),
+        c = dict(B=int(rng.integers(1, 3)), H=int(rng.choice([1, 2])), D=128, N=int(rng.integers(65536, 67000)),
                  M=int(rng.integers(0, 700)), dtype=str(rng.choice(["f32", "bf16"])), mode=str(rng.choice(MODES)),
                  seed=2000 + len(cases))
         if c["B"] * c["H"] * (-(-c["N"] // 256) + -(-c["M"] // 256)) >= 256:
@@ -68,7 +69,7 @@ def draw_wide_cases(n, seed):
     return cases
 
 
-@pytest.mark.parametrize("case", draw_wide_cases(8, 81), ids=lambda c: "B%(B)dH%(H)dN%(N)dM%(M)d-%(dtype)s-%(mode)s" % c)
+@pytest.mark.parametrize("case", draw_wide_cases(6, 81), ids=lambda c: "B%(B)dH%(H)dN%(N)dM%(M)d-%(dtype)s-%(mode)s" % c)
 def test_random_wide_d128_case(case):
     c = case
     w = Workload("random", B=c["B"], H=c["H"], D=c["D"], N=c["N"], M=c["M"], dtype=c["dtype"], seed=c["seed"])
@@ -79,6 +80,6 @@ def test_random_wide_d128_case(case):
     o_tr, o_te = o_tr.cpu().numpy(), o_te.cpu().numpy()
     ref = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"] if c["M"] else None,
                                    q_scale_mode=c["mode"])
-    rt = np.unique(np.concatenate([np.arange(0, w.N, 37), [w.N - 1]]))
-    re = np.unique(np.concatenate([np.arange(0, w.M, 23), [w.M - 1]])) if c["M"] else np.zeros(0, np.int64)
+    rt = sample_rows(w.N, 128, c["seed"])
+    re = sample_rows(w.M, 48, c["seed"] + 1) if c["M"] else np.zeros(0, np.int64)
     check_fp8_call((o_tr, o_te), ref, w.alpha, rt, re, block_kv=tfm.tfm_icl_attention_fp8_block_kv(w.D), what=c)
