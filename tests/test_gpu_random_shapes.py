@@ -55,6 +55,37 @@ def test_random_case(case):
                    block_kv=tfm.tfm_icl_attention_fp8_block_kv(w.D), what=c)
 
 
+def draw_sharp_cases(n, seed):
+    """Sharp heads: multipliers up to 8 on every tensor and 50x outlier channels (most key blocks
+    of a row then round to e4m3 zero and are skipped), up to 3000 train rows."""
+    rng = np.random.default_rng(seed)
+    cases = []
+    for i in range(n):
+        H = int(rng.integers(1, 7))
+        divisors = [g for g in range(1, H + 1) if H % g == 0]
+        cases.append(dict(B=int(rng.integers(1, 3)), H=H, D=int(rng.choice([64, 128])), N=int(rng.integers(100, 3000)),
+                          M=0 if rng.random() < 0.25 else int(rng.integers(1, 400)),
+                          dtype=str(rng.choice(["f32", "bf16"])), mode=str(rng.choice(MODES)),
+                          G=int(rng.choice(divisors)), seed=3000 + i))
+    return cases
+
+
+@pytest.mark.parametrize("case", draw_sharp_cases(12, 82), ids=lambda c: "B%(B)dH%(H)dD%(D)dN%(N)dM%(M)d-%(dtype)s-%(mode)s-G%(G)d" % c)
+def test_random_sharp_case(case):
+    c = case
+    w = Workload("sharp", B=c["B"], H=c["H"], D=c["D"], N=c["N"], M=c["M"], dtype=c["dtype"], seed=c["seed"],
+                 mult_lo=0.25, mult_hi=8.0, outlier_frac=0.005, outlier_factor=50.0)
+    x = generate(w)
+    g = gpu_inputs(x, torch.float32 if c["dtype"] == "f32" else torch.bfloat16)
+    q_test = g["q_test"] if c["M"] else None
+    o_tr, o_te = tfm.tfm_icl_attention_fp8(g["q_train"], g["k"], g["v"], q_test, alpha=w.alpha,
+                                           q_scale_mode=c["mode"], test_kv_heads=c["G"])
+    ref = OQ.quantize_qkv_per_head(x["q_train"], x["k"], x["v"], x["q_test"] if c["M"] else None,
+                                   q_scale_mode=c["mode"])
+    check_fp8_call((o_tr.cpu().numpy(), o_te.cpu().numpy()), ref, w.alpha, None, None if c["M"] else [],
+                   test_kv_heads=c["G"], block_kv=tfm.tfm_icl_attention_fp8_block_kv(w.D), what=c)
+
+
 def draw_wide_cases(n, seed):
     """Head dimension 128, at least 65536 train rows and grids of at least 256 workgroups of
     256 rows (the 8-wave kernel)."""
